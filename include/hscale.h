@@ -1,0 +1,153 @@
+/*
+ * hscale.h - C ABI of the H-Scale hot path on AMD Instinct MI355X (gfx950).
+ *
+ * H-Scale (Hessian-guided scale refinement for NVFP4) picks, for every
+ * 16-weight group of a linear layer, the E4M3 local scale that minimises the
+ * h-weighted reconstruction error, where h = diag(X^T X) comes from
+ * calibration activations X.  This library computes:
+ *
+ *   hscale_hdiag    h_j = sum_t X[t, j]^2                    (Sec. 3.2, Eq. 4)
+ *   hscale_search   the windowed E4M3 scale search per group (Sec. 3.3,
+ *                   Eq. 7 and 9-13, App. B Alg. HScaleGroupQuantize), emitting
+ *                   NVFP4 scale bytes and packed E2M1 codes
+ *   hscale_quantize the final re-quantization at given scale codes (Sec. 3.3,
+ *                   "Final re-quantization"; Eq. 12 at a fixed scale)
+ *
+ * Conventions shared by every entry point
+ *   - All pointers are device pointers (hipMalloc'd or torch CUDA tensors)
+ *     unless stated.  The caller allocates and owns every buffer; the library
+ *     allocates nothing, keeps no global state, never synchronises and is
+ *     safe to call from several host threads on different streams.
+ *   - Work is enqueued on `stream` (NULL = the default stream) and is
+ *     complete only once the caller synchronises that stream.  Arguments are
+ *     validated on the host before anything is enqueued; on any error
+ *     nothing is launched.  Kernel faults surface at the caller's next sync.
+ *   - bf16 tensors are passed as their 16-bit patterns, row-major.
+ *   - Inputs must be finite (no NaN or Inf); outputs for non-finite inputs
+ *     are unspecified.  Outputs must not overlap inputs.
+ *   - Number formats: E4M3 is OCP E4M3FN.  Scale code byte c in 1..126 is
+ *     the positive finite E4M3FN value l_c (2^-9 .. 448).  E2M1 magnitudes
+ *     are {0, 0.5, 1, 1.5, 2, 3, 4, 6}; a 4-bit code is sign << 3 | index.
+ *
+ * Arithmetic (fixed so that results are reproducible bit for bit):
+ *   S[c] = fp32(global_scale * l_c)             effective scale (Eq. 1)
+ *   R[c] = fp32(1 / S[c])                       correctly rounded
+ *   s_init = fp32(max_j |w_j| / 6)              correctly rounded (Eq. 7)
+ *   t = fp32(s_init / global_scale)             correctly rounded
+ *   c0 = clip(E4M3 round-to-nearest-even of t, saturating at 448, to 1..126)
+ *   candidate codes c = clip(c0 + d, 1, 126), d = -window .. +window
+ *   x_j = fp32(w_j * R[c]); code_j = E2M1 round-to-nearest-even of x_j
+ *     (ties to the even index, |x| > 5 -> 6), sign copied from w_j
+ *   score E(c) = sum_j h_j (w_j - v_j S[c])^2 evaluated in fp32; the first
+ *     minimum in increasing d wins
+ */
+#ifndef HSCALE_H
+#define HSCALE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hscale_status {
+    HSCALE_OK = 0,
+    HSCALE_ERR_NULL = -1,      /* a required pointer is NULL */
+    HSCALE_ERR_SHAPE = -2,     /* negative size, in % 16 != 0, or too large */
+    HSCALE_ERR_ALIGN = -3,     /* a pointer is not aligned as required */
+    HSCALE_ERR_WINDOW = -4,    /* window outside 0..125 */
+    HSCALE_ERR_SCALE = -5,     /* global_scale not finite, not > 0, or out of range */
+    HSCALE_ERR_WORKSPACE = -6, /* workspace too small */
+    HSCALE_ERR_HIP = -7,       /* the HIP runtime rejected a launch */
+    HSCALE_ERR_OVERLAP = -8,   /* an output overlaps an input */
+    HSCALE_ERR_CODE = -9       /* a scale code outside 1..126 (hscale_quantize) */
+} hscale_status;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *hscale_status_string(int status);
+
+/*
+ * Workspace size in bytes that hscale_hdiag needs for `tokens` x `in`
+ * activations: fp64 partial sums of each token slice, so that the cross-slice
+ * reduction is a fixed-order tree (deterministic, no atomics).  Depends only
+ * on (tokens, in).  Returns 0 when tokens == 0 or the sizes are invalid.
+ */
+size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in);
+
+/*
+ * The diagonal second-order proxy of Sec. 3.2, Eq. 4:
+ *     h[j] = sum_{t < tokens} X[t, j]^2,   no normalisation.
+ *
+ * X          bf16 [tokens, in], row-major, 16-byte aligned.
+ * tokens     >= 0.  tokens == 0 writes h = 0.
+ * in         >= 0, in % 16 == 0 (h is aligned with the 16-weight groups).
+ * h          fp32 [in], written.  4-byte aligned.
+ * workspace  device scratch of at least hscale_hdiag_workspace_bytes(tokens,
+ *            in) bytes, 16-byte aligned; may be NULL when that size is 0.
+ *            Its contents on entry are ignored and on exit are unspecified.
+ *
+ * Squares of bf16 values are exact in fp32.  Each lane sums at most 32
+ * tokens in fp32 before folding into fp64; slices combine in fp64 in a fixed
+ * order; h is rounded to fp32 once.  The result is within a relative 2e-6 of
+ * the exact sum and identical from run to run.
+ */
+int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
+                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The per-group NVFP4 scale search of Sec. 3.3 (Eq. 7, 9-13) with the
+ * symmetric shift set d = -window .. +window (K = 2 window + 1 candidates).
+ * window == 0 is the plain max-abs (RTN) scale of Eq. 7.
+ *
+ * W             bf16 [out, in], row-major, 16-byte aligned.  Group (r, i)
+ *               is W[r, 16 i .. 16 i + 15].
+ * out, in       out >= 0, in >= 0, in % 16 == 0.  out * in / 16 < 2^40.
+ * h             fp32 [in], the per-input-channel weights (diag of X^T X or
+ *               of a GPTQ Hessian; any h >= 0), 16-byte aligned.  The
+ *               choice is invariant to a positive scale of h.
+ * window        0 .. 125; 125 reaches every code from any start.
+ * global_scale  the FP32 tensor-level scale s_g, finite, with
+ *               s_g * 2^-9 >= 2^-126 and s_g * 448 < 2^128.  A common
+ *               choice is fp32(max|W| / 2688).
+ * scale_codes   uint8 [out, in / 16]: the chosen E4M3FN code byte per group.
+ * packed_e2m1   uint8 [out, in / 2], 8-byte aligned: the E2M1 codes at the
+ *               chosen scale, element 2k in bits 3:0 of byte k, element
+ *               2k + 1 in bits 7:4.
+ */
+int hscale_search(const void *W, int64_t out, int64_t in, const float *h,
+                  int32_t window, float global_scale, uint8_t *scale_codes,
+                  uint8_t *packed_e2m1, hipStream_t stream);
+
+/*
+ * The same search with the paper's asymmetric shift set (Eq. 9):
+ * d = -down .. +up, K = down + up + 1 (the paper uses down = 9, up = 6).
+ * hscale_search(..., window, ...) equals hscale_search_du(..., window,
+ * window, ...).  0 <= down, up <= 125.  Other arguments as hscale_search.
+ */
+int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h,
+                     int32_t down, int32_t up, float global_scale,
+                     uint8_t *scale_codes, uint8_t *packed_e2m1,
+                     hipStream_t stream);
+
+/*
+ * Final re-quantization at given scale codes (Sec. 3.3; Eq. 12 at a fixed
+ * effective scale S = s_g * l_c): packs the E2M1 codes of every group at its
+ * code byte.  Produces the same packed bytes hscale_search writes when given
+ * the codes it chose.
+ *
+ * W, out, in, global_scale, packed_e2m1   as hscale_search.
+ * scale_codes   uint8 [out, in / 16], input, each in 1..126 (checked on the
+ *               device: an out-of-range code is clamped into 1..126).
+ */
+int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale,
+                    const uint8_t *scale_codes, uint8_t *packed_e2m1,
+                    hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HSCALE_H */

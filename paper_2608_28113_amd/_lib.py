@@ -1,0 +1,94 @@
+"""ctypes binding of libhscale.so (include/hscale.h), same names as the C ABI.
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  There is no fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+LIB_PATH = Path(__file__).resolve().parent / "libhscale.so"
+
+HSCALE_OK = 0
+STATUS = {
+    0: "HSCALE_OK", -1: "HSCALE_ERR_NULL", -2: "HSCALE_ERR_SHAPE", -3: "HSCALE_ERR_ALIGN",
+    -4: "HSCALE_ERR_WINDOW", -5: "HSCALE_ERR_SCALE", -6: "HSCALE_ERR_WORKSPACE",
+    -7: "HSCALE_ERR_HIP", -8: "HSCALE_ERR_OVERLAP",
+}
+
+# Every symbol include/hscale.h declares.
+EXPORTS = (
+    "hscale_status_string",
+    "hscale_hdiag_workspace_bytes",
+    "hscale_hdiag",
+    "hscale_search",
+    "hscale_search_du",
+    "hscale_quantize",
+)
+
+_lib = None
+
+
+class HScaleError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+def load() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIB_PATH.exists():
+        raise ImportError(
+            f"{LIB_PATH} is not built; run paper_2608_28113_amd/build.py "
+            "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(str(LIB_PATH))
+    P, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    lib.hscale_status_string.argtypes = [ctypes.c_int]
+    lib.hscale_status_string.restype = ctypes.c_char_p
+    lib.hscale_hdiag_workspace_bytes.argtypes = [i64, i64]
+    lib.hscale_hdiag_workspace_bytes.restype = sz
+    lib.hscale_hdiag.argtypes = [P, i64, i64, P, P, sz, P]
+    lib.hscale_hdiag.restype = ctypes.c_int
+    lib.hscale_search.argtypes = [P, i64, i64, P, i32, f32, P, P, P]
+    lib.hscale_search.restype = ctypes.c_int
+    lib.hscale_search_du.argtypes = [P, i64, i64, P, i32, i32, f32, P, P, P]
+    lib.hscale_search_du.restype = ctypes.c_int
+    lib.hscale_quantize.argtypes = [P, i64, i64, f32, P, P, P]
+    lib.hscale_quantize.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().hscale_status_string(int(status)).decode()
+
+
+def hscale_hdiag_workspace_bytes(tokens: int, in_: int) -> int:
+    return int(load().hscale_hdiag_workspace_bytes(int(tokens), int(in_)))
+
+
+def hscale_hdiag(X: int, tokens: int, in_: int, h: int, workspace: int, workspace_bytes: int,
+                 stream: int) -> int:
+    return load().hscale_hdiag(X or None, tokens, in_, h or None, workspace or None,
+                               workspace_bytes, stream or None)
+
+
+def hscale_search(W: int, out: int, in_: int, h: int, window: int, global_scale: float,
+                  scale_codes: int, packed_e2m1: int, stream: int) -> int:
+    return load().hscale_search(W or None, out, in_, h or None, window, global_scale,
+                                scale_codes or None, packed_e2m1 or None, stream or None)
+
+
+def hscale_search_du(W: int, out: int, in_: int, h: int, down: int, up: int, global_scale: float,
+                     scale_codes: int, packed_e2m1: int, stream: int) -> int:
+    return load().hscale_search_du(W or None, out, in_, h or None, down, up, global_scale,
+                                   scale_codes or None, packed_e2m1 or None, stream or None)
+
+
+def hscale_quantize(W: int, out: int, in_: int, global_scale: float, scale_codes: int,
+                    packed_e2m1: int, stream: int) -> int:
+    return load().hscale_quantize(W or None, out, in_, global_scale, scale_codes or None,
+                                  packed_e2m1 or None, stream or None)

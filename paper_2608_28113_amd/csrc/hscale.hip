@@ -1,0 +1,502 @@
+// H-Scale hot path for gfx950: the diagonal proxy h (Sec. 3.2, Eq. 4) and the
+// per-group NVFP4 scale search (Sec. 3.3, Eq. 7, 9-13), behind the C ABI of
+// include/hscale.h.
+//
+// Kernels
+//   hdiag_partial  column sums of squares of bf16 X over one token slice.
+//                  One wave covers 512 columns (16-byte loads, 8 columns per
+//                  lane, a row segment of 1 KiB per wave); the four waves of
+//                  a block interleave rows; 8 rows of loads are in flight per
+//                  lane.  fp32 chains of at most 32 tokens fold into fp64; the
+//                  block's four waves combine through LDS in a fixed order
+//                  and one fp64 partial per (slice, column) goes to the
+//                  caller's workspace.
+//   hdiag_tree     fixed-order fp64 sum of the slice partials, one fp32 h per
+//                  column.  No atomics: results are bit-identical run to run.
+//   search         one 16-weight group per lane, lanes over consecutive
+//                  groups (a wave reads 2 KiB of W contiguously and writes
+//                  512 contiguous bytes of codes).  The 126-entry table of
+//                  (S[c], R[c]) lives in LDS.  Per candidate: 16 fp32
+//                  products w R, 8 hardware E2M1 down-conversions (packed
+//                  nibbles with sign, round-to-nearest-even, saturating at 6),
+//                  8 up-conversions back to grid values, 16 residual FMAs
+//                  w - v S (one rounding each) and a 4x4 fp32 accumulation of
+//                  h r^2.  The best candidate's packed nibbles are kept, so
+//                  the final re-quantization costs nothing extra.
+//
+// The fp32 operations below are the fixed arithmetic of the header: IEEE
+// round-to-nearest-even products, correctly rounded divisions (built with
+// -fhip-fp32-correctly-rounded-divide-sqrt), explicit fmaf, and no implicit
+// contraction (-ffp-contract=off).
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "hscale.h"
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGroup = 16;
+constexpr int kMaxCode = 126;  // positive finite E4M3FN codes are 1..126
+constexpr int kMaxWindow = 125;
+
+// ---------------------------------------------------------------------------
+// hdiag
+// ---------------------------------------------------------------------------
+constexpr int kHdThreads = 256;
+constexpr int kHdWaves = kHdThreads / 64;
+constexpr int kHdLaneCols = 8;                 // bf16 per 16-byte load
+constexpr int kHdTileCols = 64 * kHdLaneCols;  // 512 columns per block
+constexpr int kHdChunk = 32;                   // fp32 chain length per lane
+constexpr int kHdUnroll = 8;                   // row loads in flight per lane
+constexpr int kHdTargetBlocks = 4096;
+constexpr int64_t kHdMinSliceTokens = 256;
+
+struct HdiagPlan {
+    int64_t tiles = 0;
+    int64_t slices = 0;
+    int64_t slice_tokens = 0;
+};
+
+HdiagPlan hdiag_plan(int64_t tokens, int64_t in) {
+    HdiagPlan p;
+    if (tokens <= 0 || in <= 0) return p;
+    p.tiles = (in + kHdTileCols - 1) / kHdTileCols;
+    int64_t slices = (kHdTargetBlocks + p.tiles - 1) / p.tiles;
+    int64_t max_slices = (tokens + kHdMinSliceTokens - 1) / kHdMinSliceTokens;
+    if (slices > max_slices) slices = max_slices;
+    if (slices < 1) slices = 1;
+    p.slice_tokens = (tokens + slices - 1) / slices;
+    p.slices = (tokens + p.slice_tokens - 1) / p.slice_tokens;
+    return p;
+}
+
+__device__ __forceinline__ void hd_accumulate(float (&acc)[kHdLaneCols], const u32x4 &v) {
+    const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float lo = __uint_as_float(d[k] << 16);
+        const float hi = __uint_as_float(d[k] & 0xFFFF0000u);
+        acc[2 * k] = fmaf(lo, lo, acc[2 * k]);
+        acc[2 * k + 1] = fmaf(hi, hi, acc[2 * k + 1]);
+    }
+}
+
+__device__ __forceinline__ void hd_fold(float (&acc)[kHdLaneCols], double (&acc64)[kHdLaneCols]) {
+#pragma unroll
+    for (int k = 0; k < kHdLaneCols; ++k) {
+        acc64[k] += (double)acc[k];
+        acc[k] = 0.0f;
+    }
+}
+
+__global__ __launch_bounds__(kHdThreads) void hdiag_partial(const u32x4 *__restrict__ X, int64_t tokens,
+                                                            int64_t in, int64_t slice_tokens,
+                                                            double *__restrict__ partial) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t col = (int64_t)blockIdx.x * kHdTileCols + (int64_t)lane * kHdLaneCols;
+    const int64_t slice = blockIdx.y;
+    const int64_t t0 = slice * slice_tokens;
+    int64_t t1 = t0 + slice_tokens;
+    if (t1 > tokens) t1 = tokens;
+
+    double acc64[kHdLaneCols];
+    float acc[kHdLaneCols];
+#pragma unroll
+    for (int k = 0; k < kHdLaneCols; ++k) {
+        acc64[k] = 0.0;
+        acc[k] = 0.0f;
+    }
+
+    if (col < in) {
+        const int64_t vec_per_row = in / kHdLaneCols;
+        // This wave's rows: t0 + wave, t0 + wave + 4, ... < t1.
+        const int64_t first = t0 + wave;
+        const int64_t rows = first < t1 ? (t1 - first + kHdWaves - 1) / kHdWaves : 0;
+        const u32x4 *p = X + (rows > 0 ? first * vec_per_row + col / kHdLaneCols : 0);
+        const int64_t stride = (int64_t)kHdWaves * vec_per_row;
+        int64_t r = 0;
+        int since_fold = 0;
+        for (; r + kHdUnroll <= rows; r += kHdUnroll) {
+            u32x4 v[kHdUnroll];
+#pragma unroll
+            for (int u = 0; u < kHdUnroll; ++u) v[u] = __builtin_nontemporal_load(p + (r + u) * stride);
+#pragma unroll
+            for (int u = 0; u < kHdUnroll; ++u) hd_accumulate(acc, v[u]);
+            since_fold += kHdUnroll;
+            if (since_fold == kHdChunk) {
+                hd_fold(acc, acc64);
+                since_fold = 0;
+            }
+        }
+        for (; r < rows; ++r) {
+            const u32x4 v = __builtin_nontemporal_load(p + r * stride);
+            hd_accumulate(acc, v);
+        }
+        hd_fold(acc, acc64);
+    }
+
+    // Combine the four waves' column sums in a fixed order.
+    __shared__ double red[kHdWaves][kHdTileCols];
+#pragma unroll
+    for (int k = 0; k < kHdLaneCols; ++k) red[wave][lane * kHdLaneCols + k] = acc64[k];
+    __syncthreads();
+    const int c = threadIdx.x * 2;  // two columns per thread
+    const int64_t gcol = (int64_t)blockIdx.x * kHdTileCols + c;
+    if (gcol < in) {
+        double2 s;
+        s.x = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+        s.y = ((red[0][c + 1] + red[1][c + 1]) + red[2][c + 1]) + red[3][c + 1];
+        *reinterpret_cast<double2 *>(partial + slice * in + gcol) = s;
+    }
+}
+
+constexpr int kTreeCols = 64;
+constexpr int kTreeLanes = 4;
+
+__global__ __launch_bounds__(kTreeCols *kTreeLanes) void hdiag_tree(const double *__restrict__ partial,
+                                                                     int64_t slices, int64_t in,
+                                                                     float *__restrict__ h) {
+    const int lane = threadIdx.x % kTreeCols;
+    const int q = threadIdx.x / kTreeCols;
+    const int64_t col = (int64_t)blockIdx.x * kTreeCols + lane;
+    double s = 0.0;
+    if (col < in) {
+        for (int64_t k = q; k < slices; k += kTreeLanes) s += partial[k * in + col];
+    }
+    __shared__ double red[kTreeLanes][kTreeCols];
+    red[q][lane] = s;
+    __syncthreads();
+    if (q == 0 && col < in) h[col] = (float)(((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]);
+}
+
+// ---------------------------------------------------------------------------
+// Formats
+// ---------------------------------------------------------------------------
+
+// Value of a positive E4M3FN code byte c (1..126), exact in fp32:
+// exponent field 0 is subnormal (m * 2^-9), otherwise (8 + m) * 2^(e - 10).
+__device__ __forceinline__ float e4m3fn_value(int c) {
+    const int e = c >> 3;
+    const int m = c & 7;
+    return e == 0 ? (float)m * 0x1p-9f : __uint_as_float((uint32_t)((e + 120) << 23) | ((uint32_t)m << 20));
+}
+
+// E4M3FN code of a non-negative fp32 t: round to nearest, ties to the even
+// code, saturating at 448; then clipped to 1..126 (a zero or underflowing
+// group starts at the smallest code).
+__device__ __forceinline__ int e4m3fn_code_clipped(float t) {
+    // Below 2^-6 the grid is the multiples of 2^-9: t * 512 is exact.
+    const int sub = (int)__builtin_rintf(t * 512.0f);
+    // Otherwise round the fp32 pattern to 3 mantissa bits (a carry moves into
+    // the exponent) and rebias the exponent from 127 to 7.
+    const uint32_t u = __float_as_uint(t);
+    const int nrm = (int)((u + 0x7FFFFu + ((u >> 20) & 1u)) >> 20) - (120 << 3);
+    const int c = t < 0x1p-6f ? sub : nrm;
+    return min(max(c, 1), kMaxCode);
+}
+
+struct ScaleEntry {
+    float S;  // fp32(s_g * l_c)
+    float R;  // fp32(1 / S)
+};
+
+// Fills the per-block LDS table of effective scales and reciprocals.
+__device__ __forceinline__ void build_scale_table(ScaleEntry *tab, float s_g) {
+    const int c = threadIdx.x;
+    if (c <= kMaxCode + 1) {
+        const int cc = min(max(c, 1), kMaxCode);
+        const float S = s_g * e4m3fn_value(cc);
+        tab[c] = ScaleEntry{S, 1.0f / S};
+    }
+}
+
+__device__ __forceinline__ void load_group(const u32x4 *__restrict__ W, int64_t g, float (&w)[kGroup]) {
+    const u32x4 a = __builtin_nontemporal_load(W + 2 * g);
+    const u32x4 b = __builtin_nontemporal_load(W + 2 * g + 1);
+    const uint32_t d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        w[2 * k] = __uint_as_float(d[k] << 16);
+        w[2 * k + 1] = __uint_as_float(d[k] & 0xFFFF0000u);
+    }
+}
+
+// Packed E2M1 codes of 16 weights at reciprocal scale R: two 32-bit words,
+// element 2k in the low nibble of byte k.  The hardware conversion rounds to
+// nearest even, saturates at 6 and keeps the sign (scale operand 1.0: no
+// extra scaling).
+__device__ __forceinline__ uint2 quantize_group(const float (&w)[kGroup], float R) {
+    uint32_t p0 = 0, p1 = 0;
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[0] * R, w[1] * R, 1.0f, 0);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[2] * R, w[3] * R, 1.0f, 1);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[4] * R, w[5] * R, 1.0f, 2);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[6] * R, w[7] * R, 1.0f, 3);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[8] * R, w[9] * R, 1.0f, 0);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[10] * R, w[11] * R, 1.0f, 1);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[12] * R, w[13] * R, 1.0f, 2);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[14] * R, w[15] * R, 1.0f, 3);
+    return make_uint2(p0, p1);
+}
+
+// Adds the h-weighted squared residuals of elements 2K and 2K + 1 (byte K & 3
+// of word `src`) to the chains e[(2K) & 3] and e[(2K + 1) & 3].  Residuals
+// w - v S are single-rounding FMAs.
+template <int K>
+__device__ __forceinline__ void accumulate_pair(const float (&w)[kGroup], const float (&hh)[kGroup], uint32_t src,
+                                                float S, float (&e)[4]) {
+    const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, K & 3);
+    constexpr int j0 = 2 * K, j1 = 2 * K + 1;
+    const float r0 = fmaf(-v[0], S, w[j0]);
+    const float r1 = fmaf(-v[1], S, w[j1]);
+    e[j0 & 3] = fmaf(hh[j0] * r0, r0, e[j0 & 3]);
+    e[j1 & 3] = fmaf(hh[j1] * r1, r1, e[j1 & 3]);
+}
+
+// h-weighted squared error sum_j h_j (w_j - v_j S)^2 of a packed group: the
+// 16 terms go into 4 fp32 chains of 4 (j = q, q + 4, q + 8, q + 12),
+// combined as (e0 + e1) + (e2 + e3).
+__device__ __forceinline__ float group_error(const float (&w)[kGroup], const float (&hh)[kGroup], uint2 p,
+                                             float S) {
+    float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    accumulate_pair<0>(w, hh, p.x, S, e);
+    accumulate_pair<1>(w, hh, p.x, S, e);
+    accumulate_pair<2>(w, hh, p.x, S, e);
+    accumulate_pair<3>(w, hh, p.x, S, e);
+    accumulate_pair<4>(w, hh, p.y, S, e);
+    accumulate_pair<5>(w, hh, p.y, S, e);
+    accumulate_pair<6>(w, hh, p.y, S, e);
+    accumulate_pair<7>(w, hh, p.y, S, e);
+    return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+constexpr int kSearchThreads = 256;
+
+// One group per lane; a grid-stride loop over the flat group index
+// g = row * G + i (G = in / 16 groups per row), so a lane's h slice is
+// h[16 i .. 16 i + 15].
+__global__ __launch_bounds__(kSearchThreads) void search_kernel(const u32x4 *__restrict__ W,
+                                                                const float4 *__restrict__ h,
+                                                                int64_t num_groups, int64_t G, int down,
+                                                                int up, float s_g, uint8_t *__restrict__ codes,
+                                                                uint2 *__restrict__ packed) {
+    __shared__ ScaleEntry tab[kMaxCode + 2];
+    build_scale_table(tab, s_g);
+    __syncthreads();
+
+    const int64_t stride = (int64_t)gridDim.x * kSearchThreads;
+    int64_t g = (int64_t)blockIdx.x * kSearchThreads + threadIdx.x;
+    if (g >= num_groups) return;
+    int64_t i = g % G;
+    const int64_t step = stride % G;
+
+    for (; g < num_groups; g += stride) {
+        float w[kGroup];
+        load_group(W, g, w);
+        float hh[kGroup];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = h[4 * i + q];
+            hh[4 * q] = v.x;
+            hh[4 * q + 1] = v.y;
+            hh[4 * q + 2] = v.z;
+            hh[4 * q + 3] = v.w;
+        }
+
+        // Eq. 7: s_init = max|w| / 6, t = s_init / s_g, c0 = Q_fp8(t), clip.
+        float amax = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
+        const float s_init = amax / 6.0f;
+        const float t = s_init / s_g;
+        const int c0 = e4m3fn_code_clipped(t);
+
+        // Eq. 9-13: walk d = -down..up, keep the first minimum.
+        float best_e = 0.0f;
+        int best_c = 0;
+        uint2 best_p = make_uint2(0u, 0u);
+        for (int d = -down; d <= up; ++d) {
+            const int c = min(max(c0 + d, 1), kMaxCode);
+            const ScaleEntry se = tab[c];
+            const uint2 p = quantize_group(w, se.R);
+            const float e = group_error(w, hh, p, se.S);
+            if (d == -down || e < best_e) {
+                best_e = e;
+                best_c = c;
+                best_p = p;
+            }
+        }
+        codes[g] = (uint8_t)best_c;
+        packed[g] = best_p;
+
+        i += step;
+        if (i >= G) i -= G;
+    }
+}
+
+__global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *__restrict__ W,
+                                                                  int64_t num_groups, float s_g,
+                                                                  const uint8_t *__restrict__ codes,
+                                                                  uint2 *__restrict__ packed) {
+    __shared__ ScaleEntry tab[kMaxCode + 2];
+    build_scale_table(tab, s_g);
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * kSearchThreads;
+    for (int64_t g = (int64_t)blockIdx.x * kSearchThreads + threadIdx.x; g < num_groups; g += stride) {
+        float w[kGroup];
+        load_group(W, g, w);
+        const int c = min(max((int)codes[g], 1), kMaxCode);
+        packed[g] = quantize_group(w, tab[c].R);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Host side: validation and launch
+// ---------------------------------------------------------------------------
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    if (na == 0 || nb == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// True when s_g keeps every S[c] a finite normal fp32 with a finite
+// reciprocal: s_g * 2^-9 >= 2^-126 and s_g * 448 < 2^128.
+bool scale_ok(float s_g) {
+    if (!std::isfinite(s_g) || !(s_g > 0.0f)) return false;
+    const double lo = (double)s_g * std::ldexp(1.0, -9);
+    const double hi = (double)s_g * 448.0;
+    return lo >= std::ldexp(1.0, -126) && hi < std::ldexp(1.0, 128) * (1.0 - std::ldexp(1.0, -25));
+}
+
+constexpr int64_t kMaxGroups = (int64_t)1 << 40;
+
+int grid_for(int64_t groups) {
+    // Enough blocks to fill every CU several times over; the grid-stride loop
+    // covers the rest and amortises the per-block table.
+    int64_t blocks = (groups + kSearchThreads - 1) / kSearchThreads;
+    const int64_t cap = 65536;
+    if (blocks > cap) blocks = cap;
+    if (blocks < 1) blocks = 1;
+    return (int)blocks;
+}
+
+int launch_status() { return hipGetLastError() == hipSuccess ? HSCALE_OK : HSCALE_ERR_HIP; }
+
+int check_search_args(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                      float s_g, const uint8_t *codes, const uint8_t *packed) {
+    if (out < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (out > 0 && in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+    if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
+    if (!scale_ok(s_g)) return HSCALE_ERR_SCALE;
+    if (out == 0 || in == 0) return HSCALE_OK;
+    if (!W || !h || !codes || !packed) return HSCALE_ERR_NULL;
+    if (!aligned(W, 16) || !aligned(h, 16) || !aligned(packed, 8)) return HSCALE_ERR_ALIGN;
+    const size_t nw = (size_t)out * (size_t)in * 2, nh = (size_t)in * 4;
+    const size_t nc = (size_t)out * (size_t)(in / kGroup), np = (size_t)out * (size_t)(in / 2);
+    if (overlaps(codes, nc, W, nw) || overlaps(codes, nc, h, nh) || overlaps(packed, np, W, nw) ||
+        overlaps(packed, np, h, nh) || overlaps(codes, nc, packed, np))
+        return HSCALE_ERR_OVERLAP;
+    return HSCALE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hscale_status_string(int status) {
+    switch (status) {
+        case HSCALE_OK: return "HSCALE_OK";
+        case HSCALE_ERR_NULL: return "HSCALE_ERR_NULL: a required pointer is NULL";
+        case HSCALE_ERR_SHAPE: return "HSCALE_ERR_SHAPE: negative size, in % 16 != 0, or too large";
+        case HSCALE_ERR_ALIGN: return "HSCALE_ERR_ALIGN: a pointer is misaligned";
+        case HSCALE_ERR_WINDOW: return "HSCALE_ERR_WINDOW: window outside 0..125";
+        case HSCALE_ERR_SCALE: return "HSCALE_ERR_SCALE: global_scale not finite, not > 0, or out of range";
+        case HSCALE_ERR_WORKSPACE: return "HSCALE_ERR_WORKSPACE: workspace too small";
+        case HSCALE_ERR_HIP: return "HSCALE_ERR_HIP: the HIP runtime rejected a launch";
+        case HSCALE_ERR_OVERLAP: return "HSCALE_ERR_OVERLAP: an output overlaps an input";
+        default: return "unknown hscale status";
+    }
+}
+
+size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in) {
+    if (tokens <= 0 || in <= 0 || in % kGroup != 0) return 0;
+    const HdiagPlan p = hdiag_plan(tokens, in);
+    return (size_t)p.slices * (size_t)in * sizeof(double);
+}
+
+int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h, void *workspace, size_t workspace_bytes,
+                 hipStream_t stream) {
+    if (tokens < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    if (in == 0) return HSCALE_OK;
+    if (!h) return HSCALE_ERR_NULL;
+    if (!aligned(h, 4)) return HSCALE_ERR_ALIGN;
+    const HdiagPlan p = hdiag_plan(tokens, in);
+    const size_t need = hscale_hdiag_workspace_bytes(tokens, in);
+    if (tokens > 0) {
+        if (!X) return HSCALE_ERR_NULL;
+        if (!aligned(X, 16)) return HSCALE_ERR_ALIGN;
+        if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
+        if (!workspace) return HSCALE_ERR_NULL;
+        if (!aligned(workspace, 16)) return HSCALE_ERR_ALIGN;
+        const size_t nx = (size_t)tokens * (size_t)in * 2;
+        if (overlaps(h, (size_t)in * 4, X, nx) || overlaps(workspace, need, X, nx) ||
+            overlaps(workspace, need, h, (size_t)in * 4))
+            return HSCALE_ERR_OVERLAP;
+        dim3 grid((unsigned)p.tiles, (unsigned)p.slices);
+        hipLaunchKernelGGL(hdiag_partial, grid, dim3(kHdThreads), 0, stream, static_cast<const u32x4 *>(X),
+                           tokens, in, p.slice_tokens, static_cast<double *>(workspace));
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    }
+    const unsigned tree_blocks = (unsigned)((in + kTreeCols - 1) / kTreeCols);
+    hipLaunchKernelGGL(hdiag_tree, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
+                       static_cast<const double *>(workspace), p.slices, in, h);
+    return launch_status();
+}
+
+int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                     float global_scale, uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    const int st = check_search_args(W, out, in, h, down, up, global_scale, scale_codes, packed_e2m1);
+    if (st != HSCALE_OK || out == 0 || in == 0) return st;
+    const int64_t G = in / kGroup;
+    const int64_t groups = out * G;
+    hipLaunchKernelGGL(search_kernel, dim3(grid_for(groups)), dim3(kSearchThreads), 0, stream,
+                       static_cast<const u32x4 *>(W), reinterpret_cast<const float4 *>(h), groups, G, (int)down,
+                       (int)up, global_scale, scale_codes, reinterpret_cast<uint2 *>(packed_e2m1));
+    return launch_status();
+}
+
+int hscale_search(const void *W, int64_t out, int64_t in, const float *h, int32_t window, float global_scale,
+                  uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    return hscale_search_du(W, out, in, h, window, window, global_scale, scale_codes, packed_e2m1, stream);
+}
+
+int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,
+                    uint8_t *packed_e2m1, hipStream_t stream) {
+    if (out < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (out > 0 && in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+    if (!scale_ok(global_scale)) return HSCALE_ERR_SCALE;
+    if (out == 0 || in == 0) return HSCALE_OK;
+    if (!W || !scale_codes || !packed_e2m1) return HSCALE_ERR_NULL;
+    if (!aligned(W, 16) || !aligned(packed_e2m1, 8)) return HSCALE_ERR_ALIGN;
+    const size_t nw = (size_t)out * (size_t)in * 2, nc = (size_t)out * (size_t)(in / kGroup);
+    const size_t np = (size_t)out * (size_t)(in / 2);
+    if (overlaps(packed_e2m1, np, W, nw) || overlaps(packed_e2m1, np, scale_codes, nc)) return HSCALE_ERR_OVERLAP;
+    const int64_t groups = out * (in / kGroup);
+    hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(groups)), dim3(kSearchThreads), 0, stream,
+                       static_cast<const u32x4 *>(W), groups, global_scale, scale_codes,
+                       reinterpret_cast<uint2 *>(packed_e2m1));
+    return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+"""Comparison of the HIP path with the oracle (shared by the GPU tests,
+smoke() and bench.py).
+
+Bar, from the hot path's contract:
+  * h within a relative 1e-5 of the fp64 oracle (exact zeros stay zero);
+  * scale codes and packed E2M1 bytes bit-exact, given the same fp32 h, for
+    every group that is not a near-tie (the oracle's best and second-best
+    distinct-code errors within a relative 1e-6);
+  * for every group, near-ties included: the GPU's code lies in the window,
+    its packed bytes are exactly the oracle's quantization at that code, and
+    its oracle error is within the near-tie band of the oracle's minimum.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+H_REL_TOL = 1e-5
+TIE_REL = oracle.NEAR_TIE_REL
+
+
+def compare_h(h_gpu: np.ndarray, h_ref: np.ndarray) -> dict:
+    h_gpu = np.asarray(h_gpu, np.float64)
+    zero = h_ref == 0
+    rel = np.abs(h_gpu - h_ref) / np.where(zero, 1.0, h_ref)
+    return dict(max_rel=float(rel.max(initial=0.0)), zeros_exact=bool(np.all(h_gpu[zero] == 0)),
+                ok=bool(rel.max(initial=0.0) <= H_REL_TOL and np.all(h_gpu[zero] == 0)))
+
+
+def compare_search(W_bits: np.ndarray, h32: np.ndarray, s_g: float, down: int, up: int,
+                   codes_gpu: np.ndarray, packed_gpu: np.ndarray) -> dict:
+    m, n = W_bits.shape
+    G = n // 16
+    r = oracle.search(W_bits, h32, s_g, down=down, up=up)
+    tie = oracle.near_tie_mask(r["e_best"], r["e_second"])
+    codes_gpu = np.asarray(codes_gpu, np.uint8).reshape(m, G)
+    packed_gpu = np.asarray(packed_gpu, np.uint8).reshape(m, n // 2)
+    code_bad = codes_gpu != r["codes"]
+    pk_bad = np.any((packed_gpu != r["packed"]).reshape(m, G, 8), axis=-1)
+    strict_bad = (code_bad | pk_bad) & ~tie
+    # Validity of every GPU choice, near-ties included.
+    c0 = r["c0"].astype(np.int64)
+    lo = np.clip(c0 - down, 1, 126)
+    hi = np.clip(c0 + up, 1, 126)
+    cg = codes_gpu.astype(np.int64)
+    in_window = (cg >= lo) & (cg <= hi)
+    packed_at, err_at = oracle.quantize(W_bits, s_g, codes_gpu, h32)
+    packed_consistent = np.all((packed_at == packed_gpu).reshape(m, G, 8), axis=-1)
+    near_opt = err_at <= r["e_best"] + TIE_REL * r["e_second"]
+    return dict(
+        groups=int(m * G),
+        near_ties=int(tie.sum()),
+        tie_groups_differing=int(((code_bad | pk_bad) & tie).sum()),
+        mismatches=int(strict_bad.sum()),
+        outside_window=int((~in_window).sum()),
+        packed_inconsistent=int((~packed_consistent).sum()),
+        not_near_optimal=int((~near_opt).sum()),
+        ok=bool(strict_bad.sum() == 0 and in_window.all() and packed_consistent.all() and near_opt.all()),
+        oracle=r,
+    )

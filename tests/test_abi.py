@@ -1,0 +1,134 @@
+"""The C ABI loads, exports what include/hscale.h declares, and rejects bad
+arguments on the host before any launch (these run without a GPU: no path
+exercised here reaches the HIP runtime)."""
+import re
+import subprocess
+from pathlib import Path
+
+import numpy as np
+import pytest
+
+ROOT = Path(__file__).resolve().parent.parent
+HEADER = ROOT / "include" / "hscale.h"
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2608_28113_amd import _lib
+    if not _lib.LIB_PATH.exists():
+        from paper_2608_28113_amd import build
+        build.build()
+    _lib.load()
+    return _lib
+
+
+def _declared():
+    text = HEADER.read_text()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|size_t|int)\s*\**\s*(hscale_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declarations_match_binding(L):
+    assert _declared() == sorted(L.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", str(L.LIB_PATH)], capture_output=True, text=True,
+                         check=True).stdout
+    syms = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in _declared():
+        assert name in syms, name
+
+
+def test_status_strings(L):
+    for code, name in L.STATUS.items():
+        assert L.status_string(code).startswith(name)
+    assert "unknown" in L.status_string(12345)
+
+
+def test_workspace_bytes(L):
+    assert L.hscale_hdiag_workspace_bytes(0, 4096) == 0
+    assert L.hscale_hdiag_workspace_bytes(100, 15) == 0
+    assert L.hscale_hdiag_workspace_bytes(-1, 16) == 0
+    for T, n in ((128, 512), (262144, 4096), (262144, 14336), (131072, 28672), (1, 16)):
+        b = L.hscale_hdiag_workspace_bytes(T, n)
+        assert b > 0 and b % (8 * n) == 0
+        slices = b // (8 * n)
+        assert 1 <= slices <= T
+        assert b <= 0.02 * 2 * T * n or T * n < 1 << 20  # partials are a small fraction of X
+
+
+# Fake but aligned device addresses: validation never dereferences them.
+A = 1 << 20
+
+
+def test_hdiag_validation(L):
+    ws = L.hscale_hdiag_workspace_bytes(64, 32)
+    assert L.hscale_hdiag(A, 64, 33, 2 * A, 3 * A, ws, 0) == -2
+    assert L.hscale_hdiag(A, -1, 32, 2 * A, 3 * A, ws, 0) == -2
+    assert L.hscale_hdiag(A, 64, -16, 2 * A, 3 * A, ws, 0) == -2
+    assert L.hscale_hdiag(0, 64, 32, 2 * A, 3 * A, ws, 0) == -1
+    assert L.hscale_hdiag(A, 64, 32, 0, 3 * A, ws, 0) == -1
+    assert L.hscale_hdiag(A, 64, 32, 2 * A, 0, ws, 0) == -1
+    assert L.hscale_hdiag(A + 8, 64, 32, 2 * A, 3 * A, ws, 0) == -3
+    assert L.hscale_hdiag(A, 64, 32, 2 * A + 2, 3 * A, ws, 0) == -3
+    assert L.hscale_hdiag(A, 64, 32, 2 * A, 3 * A + 8, ws, 0) == -3
+    assert L.hscale_hdiag(A, 64, 32, 2 * A, 3 * A, ws - 1, 0) == -6
+    # h inside X, workspace inside X
+    assert L.hscale_hdiag(A, 64, 32, A + 64, 3 * A, ws, 0) == -8
+    assert L.hscale_hdiag(A, 64, 32, 2 * A, A + 1024, ws, 0) == -8
+    # in == 0 is a no-op
+    assert L.hscale_hdiag(0, 64, 0, 0, 0, 0, 0) == 0
+
+
+def test_search_validation(L):
+    m, n = 4, 64
+    W, h, codes, packed = A, 2 * A, 3 * A, 4 * A
+    ok = dict(W=W, h=h, codes=codes, packed=packed)
+
+    def call(W=W, out=m, in_=n, h=h, window=4, s=1e-3, codes=codes, packed=packed):
+        return L.hscale_search(W, out, in_, h, window, s, codes, packed, 0)
+
+    assert call(in_=65) == -2
+    assert call(out=-1) == -2
+    assert call(in_=-16) == -2
+    assert call(out=1 << 40, in_=1 << 10) == -2
+    assert call(window=-1) == -4
+    assert call(window=126) == -4
+    for s in (0.0, -1.0, float("inf"), float("nan"), 1e-40, 2.0 ** -118, 1e36):
+        assert call(s=s) == -5, s
+    assert call(W=0) == -1
+    assert call(h=0) == -1
+    assert call(codes=0) == -1
+    assert call(packed=0) == -1
+    assert call(W=W + 2) == -3
+    assert call(h=h + 4) == -3
+    assert call(packed=packed + 4) == -3
+    assert call(codes=W + 16) == -8
+    assert call(packed=h) == -8
+    assert call(codes=packed + 8) == -8
+    # empty problems are no-ops (no pointer needed)
+    assert L.hscale_search(0, 0, n, 0, 4, 1e-3, 0, 0, 0) == 0
+    assert L.hscale_search(0, m, 0, 0, 4, 1e-3, 0, 0, 0) == 0
+    assert L.hscale_search_du(W, m, n, h, 9, 126, 1e-3, codes, packed, 0) == -4
+    assert L.hscale_search_du(W, m, n, h, -1, 6, 1e-3, codes, packed, 0) == -4
+
+
+def test_quantize_validation(L):
+    m, n = 4, 64
+    W, codes, packed = A, 2 * A, 3 * A
+    assert L.hscale_quantize(W, m, 17, 1e-3, codes, packed, 0) == -2
+    assert L.hscale_quantize(W, m, n, 0.0, codes, packed, 0) == -5
+    assert L.hscale_quantize(0, m, n, 1e-3, codes, packed, 0) == -1
+    assert L.hscale_quantize(W, m, n, 1e-3, 0, packed, 0) == -1
+    assert L.hscale_quantize(W + 4, m, n, 1e-3, codes, packed, 0) == -3
+    assert L.hscale_quantize(W, m, n, 1e-3, codes, W + 32, 0) == -8
+    assert L.hscale_quantize(0, 0, n, 1e-3, 0, 0, 0) == 0
+
+
+def test_torch_front_end_rejects_bad_tensors():
+    import torch
+    from paper_2608_28113_amd import ops
+    with pytest.raises(ValueError):
+        ops.hdiag(torch.zeros(4, 16, dtype=torch.float32))
+    with pytest.raises(ValueError):
+        ops.search(torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(16), 1e-3, window=4)
