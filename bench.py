@@ -44,6 +44,34 @@ def search_ops_per_weight(K: int) -> int:
     return 5 * K + 3
 
 
+PROFILE_JSON = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "down_proj_4096x14336_t262144_w4.json")
+KERNEL_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_28113_amd", "csrc",
+                          "hscale.hip")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary (copy-calibrated), or None when that summary was taken on another
+    workload or before the kernels last changed."""
+    import hashlib
+    if workload != "down_proj" or not os.path.exists(PROFILE_JSON):
+        return None
+    with open(PROFILE_JSON) as f:
+        prof = json.load(f)
+    with open(KERNEL_SRC, "rb") as f:
+        src = hashlib.sha256(f.read()).hexdigest()[:16]
+    if prof.get("kernel_source_sha256_16") != src:
+        return None
+    t = prof.get("traffic", {})
+
+    def tot(*names):
+        if not all(n in t for n in names):
+            return None
+        return sum(t[n]["read_bytes"] + t[n]["write_bytes"] for n in names)
+    return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot("search_kernel")}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -58,6 +86,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-mode", action="store_true",
                     help="only warm-up and timed steps (for rocprofv3 runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy, a kernel of known traffic "
+                         "for scaling the HBM byte counters")
     return ap.parse_args()
 
 
@@ -122,6 +153,14 @@ def main():
     t_h = np.array([e[0].elapsed_time(e[1]) for e in events]) * 1e-3
     t_s = np.array([e[1].elapsed_time(e[2]) for e in events]) * 1e-3
     t_step = np.array([e[0].elapsed_time(e[2]) for e in events]) * 1e-3
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if args.profile_mode:
         print(json.dumps({"profile_mode": True, "hdiag_ms": float(t_h.mean() * 1e3),
                           "search_ms": float(t_s.mean() * 1e3)}), flush=True)
@@ -145,6 +184,12 @@ def main():
                  "algorithmic_ops_per_launch": ops, "ops_per_weight": search_ops_per_weight(K),
                  "hbm_GBps": round(search_gbs, 1), "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4),
                  "avg_launch_ms": round(t_s.mean() * 1e3, 4)}
+    traffic = measured_traffic(wl.name if window == 4 else "")
+    if traffic:
+        rl_hdiag["traffic"] = traffic["hdiag"]
+        rl_search["traffic"] = traffic["search"]
+        rl_hdiag["traffic_source"] = rl_search["traffic_source"] = os.path.relpath(
+            PROFILE_JSON, os.path.dirname(os.path.abspath(__file__)))
     dominant = rl_hdiag if t_h.mean() >= t_s.mean() else rl_search
 
     out = {
