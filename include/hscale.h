@@ -62,8 +62,7 @@ typedef enum hscale_status {
     HSCALE_ERR_SCALE = -5,     /* global_scale not finite, not > 0, or out of range */
     HSCALE_ERR_WORKSPACE = -6, /* workspace too small */
     HSCALE_ERR_HIP = -7,       /* the HIP runtime rejected a launch */
-    HSCALE_ERR_OVERLAP = -8,   /* an output overlaps an input */
-    HSCALE_ERR_CODE = -9       /* a scale code outside 1..126 (hscale_quantize) */
+    HSCALE_ERR_OVERLAP = -8    /* an output overlaps an input */
 } hscale_status;
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -104,7 +103,8 @@ int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
  *
  * W             bf16 [out, in], row-major, 16-byte aligned.  Group (r, i)
  *               is W[r, 16 i .. 16 i + 15].
- * out, in       out >= 0, in >= 0, in % 16 == 0.  out * in / 16 < 2^40.
+ * out, in       out >= 0, in >= 0, in % 16 == 0, and fewer than 2^32
+ *               groups (out * in / 16), which are indexed in 32 bits.
  * h             fp32 [in], the per-input-channel weights (diag of X^T X or
  *               of a GPTQ Hessian; any h >= 0), 16-byte aligned.  The
  *               choice is invariant to a positive scale of h.
@@ -139,8 +139,8 @@ int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h,
  * the codes it chose.
  *
  * W, out, in, global_scale, packed_e2m1   as hscale_search.
- * scale_codes   uint8 [out, in / 16], input, each in 1..126 (checked on the
- *               device: an out-of-range code is clamped into 1..126).
+ * scale_codes   uint8 [out, in / 16], input, each in 1..126; a byte
+ *               outside that range is treated as the nearest of 1 and 126.
  */
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale,
                     const uint8_t *scale_codes, uint8_t *packed_e2m1,

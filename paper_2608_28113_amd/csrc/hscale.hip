@@ -208,14 +208,25 @@ struct ScaleEntry {
     float R;  // fp32(1 / S)
 };
 
-// Fills the per-block LDS table of effective scales and reciprocals.
-__device__ __forceinline__ void build_scale_table(ScaleEntry *tab, float s_g) {
+// The search indexes its table by c0 + d + kTabPad with no clamp: entries
+// below kTabPad + 1 hold code 1 and entries above kTabPad + 126 hold code 126,
+// which is the clip of Eq. 10.  c0 is in 1..126 and |d| <= 125, so the index
+// stays in 1..376.
+constexpr int kTabPad = kMaxWindow;
+constexpr int kTabSize = 384;
+
+// Fills a padded LDS table: tab[t] = (S, R) of code clip(t - kTabPad, 1, 126).
+// The 126 distinct entries are computed once (one correctly rounded
+// reciprocal each) into `uniq`, then copied out.  Needs blockDim.x >= 128.
+__device__ __forceinline__ void build_scale_table(ScaleEntry *tab, ScaleEntry *uniq, float s_g) {
     const int c = threadIdx.x;
-    if (c <= kMaxCode + 1) {
-        const int cc = min(max(c, 1), kMaxCode);
-        const float S = s_g * e4m3fn_value(cc);
-        tab[c] = ScaleEntry{S, 1.0f / S};
+    if (c >= 1 && c <= kMaxCode) {
+        const float S = s_g * e4m3fn_value(c);
+        uniq[c] = ScaleEntry{S, 1.0f / S};
     }
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTabSize; t += blockDim.x) tab[t] = uniq[min(max(t - kTabPad, 1), kMaxCode)];
+    __syncthreads();
 }
 
 __device__ __forceinline__ void load_group(const u32x4 *__restrict__ W, int64_t g, float (&w)[kGroup]) {
@@ -233,8 +244,9 @@ __device__ __forceinline__ void load_group(const u32x4 *__restrict__ W, int64_t 
 // element 2k in the low nibble of byte k.  The hardware conversion rounds to
 // nearest even, saturates at 6 and keeps the sign (scale operand 1.0: no
 // extra scaling).
-__device__ __forceinline__ uint2 quantize_group(const float (&w)[kGroup], float R) {
-    uint32_t p0 = 0, p1 = 0;
+__device__ __forceinline__ uint2 quantize_group(const float (&w)[kGroup], float R, uint2 old) {
+    // Every byte of both words is overwritten, so `old` only saves a move.
+    uint32_t p0 = old.x, p1 = old.y;
     p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[0] * R, w[1] * R, 1.0f, 0);
     p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[2] * R, w[3] * R, 1.0f, 1);
     p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[4] * R, w[5] * R, 1.0f, 2);
@@ -279,25 +291,77 @@ __device__ __forceinline__ float group_error(const float (&w)[kGroup], const flo
 
 constexpr int kSearchThreads = 256;
 
-// One group per lane; a grid-stride loop over the flat group index
-// g = row * G + i (G = in / 16 groups per row), so a lane's h slice is
-// h[16 i .. 16 i + 15].
+// Eq. 7 and 9-13 for one group held in registers: the max-abs initial code,
+// then the walk d = -down..up in pairs, keeping the first minimum.
+__device__ __forceinline__ void search_group(const float (&w)[kGroup], const float (&hh)[kGroup],
+                                             const ScaleEntry *tab, int down, int up, float s_g, int &code,
+                                             uint2 &best_p) {
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
+    const float s_init = amax / 6.0f;
+    const float t = s_init / s_g;
+    const int c0 = e4m3fn_code_clipped(t);
+    const ScaleEntry *col = tab + (c0 + kTabPad);  // col[d] is candidate c0 + d, clipped
+    float best_e = 0.0f;
+    int best_d = -down;
+    best_p = make_uint2(0u, 0u);
+    // Scratch words the conversions rewrite in place (all 8 bytes each time),
+    // carried across iterations so no register copies are needed.
+    uint2 pa = best_p, pb = best_p;
+    int d = -down;
+    for (; d < up; d += 2) {
+        const ScaleEntry sa = col[d];
+        const ScaleEntry sb = col[d + 1];
+        pa = quantize_group(w, sa.R, pa);
+        pb = quantize_group(w, sb.R, pb);
+        const float ea = group_error(w, hh, pa, sa.S);
+        const float eb = group_error(w, hh, pb, sb.S);
+        if (d == -down || ea < best_e) {
+            best_e = ea;
+            best_d = d;
+            best_p = pa;
+        }
+        if (eb < best_e) {
+            best_e = eb;
+            best_d = d + 1;
+            best_p = pb;
+        }
+    }
+    if (d == up) {  // odd candidate count: the last one
+        const ScaleEntry se = col[d];
+        pa = quantize_group(w, se.R, pa);
+        const float e = group_error(w, hh, pa, se.S);
+        if (d == -down || e < best_e) {
+            best_e = e;
+            best_d = d;
+            best_p = pa;
+        }
+    }
+    code = min(max(c0 + best_d, 1), kMaxCode);
+}
+
+// One group per lane over the flat group index g = row * G + i (G = in / 16
+// groups per row), so a lane's h slice is h[16 i .. 16 i + 15].  A launch
+// normally covers every group once; larger problems loop with a grid stride.
 __global__ __launch_bounds__(kSearchThreads) void search_kernel(const u32x4 *__restrict__ W,
                                                                 const float4 *__restrict__ h,
-                                                                int64_t num_groups, int64_t G, int down,
+                                                                uint32_t num_groups, uint32_t G, int down,
                                                                 int up, float s_g, uint8_t *__restrict__ codes,
                                                                 uint2 *__restrict__ packed) {
-    __shared__ ScaleEntry tab[kMaxCode + 2];
-    build_scale_table(tab, s_g);
-    __syncthreads();
+    __shared__ ScaleEntry tab[kTabSize];
+    __shared__ ScaleEntry uniq[kMaxCode + 1];
+    build_scale_table(tab, uniq, s_g);
 
-    const int64_t stride = (int64_t)gridDim.x * kSearchThreads;
-    int64_t g = (int64_t)blockIdx.x * kSearchThreads + threadIdx.x;
+    const uint32_t stride = gridDim.x * kSearchThreads;
+    const uint32_t first = blockIdx.x * kSearchThreads;  // wave-uniform
+    uint32_t g = first + threadIdx.x;
     if (g >= num_groups) return;
-    int64_t i = g % G;
-    const int64_t step = stride % G;
+    uint32_t i = first % G + threadIdx.x;  // column group of g
+    while (i >= G) i -= G;
+    const uint32_t step = stride % G;
 
-    for (; g < num_groups; g += stride) {
+    for (;;) {
         float w[kGroup];
         load_group(W, g, w);
         float hh[kGroup];
@@ -309,33 +373,14 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const u32x4 *__r
             hh[4 * q + 2] = v.z;
             hh[4 * q + 3] = v.w;
         }
-
-        // Eq. 7: s_init = max|w| / 6, t = s_init / s_g, c0 = Q_fp8(t), clip.
-        float amax = 0.0f;
-#pragma unroll
-        for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
-        const float s_init = amax / 6.0f;
-        const float t = s_init / s_g;
-        const int c0 = e4m3fn_code_clipped(t);
-
-        // Eq. 9-13: walk d = -down..up, keep the first minimum.
-        float best_e = 0.0f;
-        int best_c = 0;
-        uint2 best_p = make_uint2(0u, 0u);
-        for (int d = -down; d <= up; ++d) {
-            const int c = min(max(c0 + d, 1), kMaxCode);
-            const ScaleEntry se = tab[c];
-            const uint2 p = quantize_group(w, se.R);
-            const float e = group_error(w, hh, p, se.S);
-            if (d == -down || e < best_e) {
-                best_e = e;
-                best_c = c;
-                best_p = p;
-            }
-        }
-        codes[g] = (uint8_t)best_c;
+        int code;
+        uint2 best_p;
+        search_group(w, hh, tab, down, up, s_g, code, best_p);
+        codes[g] = (uint8_t)code;
         packed[g] = best_p;
 
+        if (num_groups - g <= stride) break;
+        g += stride;
         i += step;
         if (i >= G) i -= G;
     }
@@ -345,15 +390,15 @@ __global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *_
                                                                   int64_t num_groups, float s_g,
                                                                   const uint8_t *__restrict__ codes,
                                                                   uint2 *__restrict__ packed) {
-    __shared__ ScaleEntry tab[kMaxCode + 2];
-    build_scale_table(tab, s_g);
-    __syncthreads();
+    __shared__ ScaleEntry tab[kTabSize];
+    __shared__ ScaleEntry uniq[kMaxCode + 1];
+    build_scale_table(tab, uniq, s_g);
     const int64_t stride = (int64_t)gridDim.x * kSearchThreads;
     for (int64_t g = (int64_t)blockIdx.x * kSearchThreads + threadIdx.x; g < num_groups; g += stride) {
         float w[kGroup];
         load_group(W, g, w);
         const int c = min(max((int)codes[g], 1), kMaxCode);
-        packed[g] = quantize_group(w, tab[c].R);
+        packed[g] = quantize_group(w, tab[c + kTabPad].R, make_uint2(0u, 0u));
     }
 }
 
@@ -378,7 +423,8 @@ bool scale_ok(float s_g) {
     return lo >= std::ldexp(1.0, -126) && hi < std::ldexp(1.0, 128) * (1.0 - std::ldexp(1.0, -25));
 }
 
-constexpr int64_t kMaxGroups = (int64_t)1 << 40;
+// The search indexes groups with 32-bit arithmetic.
+constexpr int64_t kMaxGroups = ((int64_t)1 << 32) - 1;
 
 int grid_for(int64_t groups) {
     // Enough blocks to fill every CU several times over; the grid-stride loop
@@ -471,8 +517,9 @@ int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h, int
     const int64_t G = in / kGroup;
     const int64_t groups = out * G;
     hipLaunchKernelGGL(search_kernel, dim3(grid_for(groups)), dim3(kSearchThreads), 0, stream,
-                       static_cast<const u32x4 *>(W), reinterpret_cast<const float4 *>(h), groups, G, (int)down,
-                       (int)up, global_scale, scale_codes, reinterpret_cast<uint2 *>(packed_e2m1));
+                       static_cast<const u32x4 *>(W), reinterpret_cast<const float4 *>(h), (uint32_t)groups,
+                       (uint32_t)G, (int)down, (int)up, global_scale, scale_codes,
+                       reinterpret_cast<uint2 *>(packed_e2m1));
     return launch_status();
 }
 
