@@ -55,7 +55,11 @@ constexpr int kHdLaneCols = 8;                 // bf16 per 16-byte load
 constexpr int kHdTileCols = 64 * kHdLaneCols;  // 512 columns per block
 constexpr int kHdChunk = 32;                   // fp32 chain length per lane
 constexpr int kHdUnroll = 8;                   // row loads in flight per lane
-constexpr int kHdTargetBlocks = 4096;
+// Grid size: as many blocks as MI355X keeps resident at once (256 CUs x 7
+// blocks of 4 waves at this kernel's 68 VGPRs), so the whole grid runs in
+// one round with no tail.  The plan depends only on (tokens, in), which
+// keeps results identical from run to run.
+constexpr int kHdTargetBlocks = 1792;
 constexpr int64_t kHdMinSliceTokens = 256;
 
 struct HdiagPlan {
@@ -68,7 +72,7 @@ HdiagPlan hdiag_plan(int64_t tokens, int64_t in) {
     HdiagPlan p;
     if (tokens <= 0 || in <= 0) return p;
     p.tiles = (in + kHdTileCols - 1) / kHdTileCols;
-    int64_t slices = (kHdTargetBlocks + p.tiles - 1) / p.tiles;
+    int64_t slices = kHdTargetBlocks / p.tiles;
     int64_t max_slices = (tokens + kHdMinSliceTokens - 1) / kHdMinSliceTokens;
     if (slices > max_slices) slices = max_slices;
     if (slices < 1) slices = 1;
