@@ -72,6 +72,11 @@ def _load():
     lib.oracle_search.argtypes = [P, i64, i64, P, ctypes.c_int, ctypes.c_int,
                                   ctypes.c_float, P, P, P, P, P]
     lib.oracle_search.restype = ctypes.c_int
+    lib.oracle_search_init.argtypes = [P, i64, i64, P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                       ctypes.c_int, P, P, P, P, P, P, P, P]
+    lib.oracle_search_init.restype = ctypes.c_int
+    lib.oracle_hdiag_accumulate.argtypes = [P, i64, i64, P]
+    lib.oracle_hdiag_accumulate.restype = None
     lib.oracle_quantize.argtypes = [P, i64, i64, ctypes.c_float, P, P, P, P]
     lib.oracle_quantize.restype = ctypes.c_int
     lib.oracle_all_code_errors.argtypes = [P, i64, i64, P, ctypes.c_float, P]
@@ -147,13 +152,19 @@ def hdiag(X) -> np.ndarray:
     return h
 
 
+INIT_RTN, INIT_4OVER6, INIT_GIVEN = 0, 1, 2
+
+
 def search(W, h, s_g: float, window: int | None = None, down: int | None = None,
-           up: int | None = None) -> dict:
+           up: int | None = None, init="rtn") -> dict:
     """The windowed scale search over a [m, n] bf16 matrix.
 
     Either ``window`` (symmetric, shifts -window..+window) or ``down``/``up``.
+    ``init`` is "rtn" (max-abs, Eq. 7), "4over6" (the better of max/4 and
+    max/6 under plain MSE), or a uint8 array [m, n/16] of initial codes.
     Returns codes [m, n/16] u8, packed [m, n/2] u8, e_best / e_second
-    [m, n/16] f64 and c0 [m, n/16] u8.
+    [m, n/16] f64, c0 [m, n/16] u8 (the initial codes) and, for "4over6",
+    l4 / l6 [m, n/16] f64 (the two anchors' plain squared errors).
     """
     if window is not None:
         down = up = int(window)
@@ -162,17 +173,39 @@ def search(W, h, s_g: float, window: int | None = None, down: int | None = None,
     h = np.ascontiguousarray(h, dtype=np.float32)
     assert h.shape == (n,)
     G = n // 16
+    init_codes = None
+    if isinstance(init, str):
+        mode = {"rtn": INIT_RTN, "4over6": INIT_4OVER6}[init]
+    else:
+        mode = INIT_GIVEN
+        init_codes = np.ascontiguousarray(init, dtype=np.uint8)
+        assert init_codes.shape == (m, G)
     codes = np.zeros((m, G), np.uint8)
     packed = np.zeros((m, n // 2), np.uint8)
     e_best = np.zeros((m, G), np.float64)
     e_second = np.zeros((m, G), np.float64)
     c0 = np.zeros((m, G), np.uint8)
-    rc = _load().oracle_search(_ptr(W), m, n, _ptr(h), int(down), int(up),
-                               np.float32(s_g), _ptr(codes), _ptr(packed),
-                               _ptr(e_best), _ptr(e_second), _ptr(c0))
+    l4 = np.zeros((m, G), np.float64)
+    l6 = np.zeros((m, G), np.float64)
+    rc = _load().oracle_search_init(_ptr(W), m, n, _ptr(h), int(down), int(up),
+                                    np.float32(s_g), mode, _ptr(init_codes), _ptr(codes),
+                                    _ptr(packed), _ptr(e_best), _ptr(e_second), _ptr(c0),
+                                    _ptr(l4), _ptr(l6))
     if rc != 0:
-        raise ValueError("oracle_search: bad arguments")
-    return dict(codes=codes, packed=packed, e_best=e_best, e_second=e_second, c0=c0)
+        raise ValueError("oracle_search_init: bad arguments")
+    out = dict(codes=codes, packed=packed, e_best=e_best, e_second=e_second, c0=c0)
+    if mode == INIT_4OVER6:
+        out.update(l4=l4, l6=l6)
+    return out
+
+
+def hdiag_accumulate(X, h64: np.ndarray) -> np.ndarray:
+    """h64 += sum_t X[t, :]^2 in place (fp64), for streamed calibration."""
+    X = _bf16_bits(X)
+    T, n = X.shape
+    assert h64.dtype == np.float64 and h64.shape == (n,) and h64.flags["C_CONTIGUOUS"]
+    _load().oracle_hdiag_accumulate(_ptr(X), T, n, _ptr(h64))
+    return h64
 
 
 def quantize(W, s_g: float, codes, h=None):

@@ -166,18 +166,17 @@ double oracle_quantize_group(const double *w, const int *neg, const double *h,
     return err;
 }
 
-/* Windowed search for one group of g weights.  Candidate codes are
- * clip(c0 + d, 1, M) for d = -down..up in increasing d (Eq. 9-10); each is
- * scored with Eq. 13; the first minimum wins.  Outputs: chosen code, its
- * nibbles, its error, the smallest error over candidate codes other than the
- * chosen one (INFINITY when every candidate is the chosen code), and c0.
+/* The walk of Eq. 9-13 from a given initial ladder index c0 (Alg.
+ * HScaleGroupQuantize takes the baseline's initial scale as an input).
+ * Candidate codes are clip(c0 + d, 1, M) for d = -down..up in increasing d;
+ * each is scored with Eq. 13; the first minimum wins.  Outputs: chosen code,
+ * its nibbles, its error, and the smallest error over candidate codes other
+ * than the chosen one (INFINITY when every candidate is the chosen code).
  * cand_codes / cand_err, when non-NULL, receive all down+up+1 candidates. */
-int oracle_search_group(const double *w, const int *neg, const double *h,
-                        int g, float s_g, int down, int up, const float *S,
-                        const float *R, uint8_t *nib_out, double *e_best,
-                        double *e_second, int *c0_out, int *cand_codes,
-                        double *cand_err) {
-    int c0 = oracle_init_code_f(w, g, s_g);
+int oracle_walk_group(const double *w, const int *neg, const double *h, int g,
+                      int c0, int down, int up, const float *S,
+                      const float *R, uint8_t *nib_out, double *e_best,
+                      double *e_second, int *cand_codes, double *cand_err) {
     int best_c = 0;
     double best_e = 0.0;
     int k = 0;
@@ -206,8 +205,50 @@ int oracle_search_group(const double *w, const int *neg, const double *h,
     oracle_quantize_group(w, neg, h, g, S[best_c], R[best_c], nib_out);
     if (e_best) *e_best = best_e;
     if (e_second) *e_second = second;
-    if (c0_out) *c0_out = c0;
     return best_c;
+}
+
+/* Windowed search for one group from the max-abs (RTN) initial code. */
+int oracle_search_group(const double *w, const int *neg, const double *h,
+                        int g, float s_g, int down, int up, const float *S,
+                        const float *R, uint8_t *nib_out, double *e_best,
+                        double *e_second, int *c0_out, int *cand_codes,
+                        double *cand_err) {
+    int c0 = oracle_init_code_f(w, g, s_g);
+    if (c0_out) *c0_out = c0;
+    return oracle_walk_group(w, neg, h, g, c0, down, up, S, R, nib_out,
+                             e_best, e_second, cand_codes, cand_err);
+}
+
+/* The 4over6 initialisation (App. B, Alg. combining 4over6 with H-Scale):
+ * for each anchor a in (4, 6), s_a = max|w| / a in fp32, l_a = Q_fp8(s_a /
+ * s_g) in fp32 (clipped to the ladder as in Eq. 10), quantize the group at
+ * s_g l_a and score the plain squared error; the initial code is the anchor
+ * with the smaller error, the first anchor (4) on a tie.  L4 / L6 and the
+ * two anchor codes are returned for reporting. */
+int oracle_init_code_4over6(const double *w, const int *neg, int g, float s_g,
+                            const float *S, const float *R, double *L4,
+                            double *L6, int *c4_out, int *c6_out) {
+    static const double anchors[2] = {4.0, 6.0};
+    double amax = 0.0;
+    for (int j = 0; j < g; ++j)
+        if (fabs(w[j]) > amax) amax = fabs(w[j]);
+    int code[2];
+    double loss[2];
+    for (int a = 0; a < 2; ++a) {
+        double s_a = rn32(amax / anchors[a]);
+        double t = rn32(s_a / (double)s_g);
+        int c = oracle_e4m3_round(t);
+        if (c < 1) c = 1;
+        if (c > ORACLE_M) c = ORACLE_M;
+        code[a] = c;
+        loss[a] = oracle_quantize_group(w, neg, NULL, g, S[c], R[c], NULL);
+    }
+    if (L4) *L4 = loss[0];
+    if (L6) *L6 = loss[1];
+    if (c4_out) *c4_out = code[0];
+    if (c6_out) *c6_out = code[1];
+    return loss[0] <= loss[1] ? code[0] : code[1];
 }
 
 /* ------------------------------------------------------------------------
@@ -217,6 +258,19 @@ int oracle_search_group(const double *w, const int *neg, const double *h,
 /* Eq. 4: h_j = sum_t X[t, j]^2, in fp64, no normalisation. */
 void oracle_hdiag(const uint16_t *X, int64_t tokens, int64_t n, double *h) {
     for (int64_t j = 0; j < n; ++j) h[j] = 0.0;
+    for (int64_t t = 0; t < tokens; ++t) {
+        const uint16_t *row = X + t * n;
+        for (int64_t j = 0; j < n; ++j) {
+            double x = bf16_value(row[j]);
+            h[j] += x * x;
+        }
+    }
+}
+
+/* Streamed calibration: h[j] += sum_t X[t, j]^2 into an fp64 accumulator
+ * (Eq. 4 over the concatenation of every batch passed in). */
+void oracle_hdiag_accumulate(const uint16_t *X, int64_t tokens, int64_t n,
+                             double *h) {
     for (int64_t t = 0; t < tokens; ++t) {
         const uint16_t *row = X + t * n;
         for (int64_t j = 0; j < n; ++j) {
@@ -243,15 +297,25 @@ static void store_nibbles(uint8_t *packed, int64_t n, int64_t r, int64_t i,
         dst[k] = (uint8_t)(nib[2 * k] | (nib[2 * k + 1] << 4));
 }
 
+/* Initial-code rules for the matrix-level search. */
+#define ORACLE_INIT_RTN 0      /* max-abs scale, Eq. 7 */
+#define ORACLE_INIT_4OVER6 1   /* the better of max/4 and max/6 (plain MSE) */
+#define ORACLE_INIT_GIVEN 2    /* caller-provided code per group */
+
 /* The search over a whole m x n matrix (n % 16 == 0) with shift set
- * {-down..up}.  codes: [m, n/16] E4M3 bytes; packed: [m, n/2] bytes.
- * e_best / e_second / c0 (optional, [m, n/16]) support near-tie reports.
- * Returns 0, or -1 on a bad argument. */
-int oracle_search(const uint16_t *W, int64_t m, int64_t n, const float *h,
-                  int down, int up, float s_g, uint8_t *codes,
-                  uint8_t *packed, double *e_best, double *e_second,
-                  uint8_t *c0) {
+ * {-down..up} and the given initial-code rule.  codes: [m, n/16] E4M3
+ * bytes; packed: [m, n/2] bytes.  init_codes ([m, n/16]) is read for
+ * ORACLE_INIT_GIVEN.  e_best / e_second / c0 / l4 / l6 (optional,
+ * [m, n/16]) support near-tie reports; l4 / l6 are only written for
+ * ORACLE_INIT_4OVER6.  Returns 0, or -1 on a bad argument. */
+int oracle_search_init(const uint16_t *W, int64_t m, int64_t n, const float *h,
+                       int down, int up, float s_g, int init_mode,
+                       const uint8_t *init_codes, uint8_t *codes,
+                       uint8_t *packed, double *e_best, double *e_second,
+                       uint8_t *c0, double *l4, double *l6) {
     if (n % 16 != 0 || down < 0 || up < 0 || !(s_g > 0.0f)) return -1;
+    if (init_mode < 0 || init_mode > 2) return -1;
+    if (init_mode == ORACLE_INIT_GIVEN && !init_codes) return -1;
     float S[ORACLE_M + 1], R[ORACLE_M + 1];
     oracle_scale_tables(s_g, S, R);
     int64_t G = n / 16;
@@ -262,18 +326,40 @@ int oracle_search(const uint16_t *W, int64_t m, int64_t n, const float *h,
         for (int64_t i = 0; i < G; ++i) {
             load_group(W, n, r, i, w, neg);
             for (int j = 0; j < 16; ++j) hh[j] = (double)h[i * 16 + j];
-            double eb, es;
             int c0v;
-            int c = oracle_search_group(w, neg, hh, 16, s_g, down, up, S, R,
-                                        nib, &eb, &es, &c0v, NULL, NULL);
+            double L4 = 0.0, L6 = 0.0;
+            if (init_mode == ORACLE_INIT_RTN) {
+                c0v = oracle_init_code_f(w, 16, s_g);
+            } else if (init_mode == ORACLE_INIT_4OVER6) {
+                c0v = oracle_init_code_4over6(w, neg, 16, s_g, S, R, &L4, &L6,
+                                              NULL, NULL);
+            } else {
+                c0v = init_codes[r * G + i];
+                if (c0v < 1) c0v = 1;
+                if (c0v > ORACLE_M) c0v = ORACLE_M;
+            }
+            double eb, es;
+            int c = oracle_walk_group(w, neg, hh, 16, c0v, down, up, S, R, nib,
+                                      &eb, &es, NULL, NULL);
             codes[r * G + i] = (uint8_t)c;
             store_nibbles(packed, n, r, i, nib);
             if (e_best) e_best[r * G + i] = eb;
             if (e_second) e_second[r * G + i] = es;
             if (c0) c0[r * G + i] = (uint8_t)c0v;
+            if (l4 && init_mode == ORACLE_INIT_4OVER6) l4[r * G + i] = L4;
+            if (l6 && init_mode == ORACLE_INIT_4OVER6) l6[r * G + i] = L6;
         }
     }
     return 0;
+}
+
+/* The search from the max-abs initial code (Eq. 7). */
+int oracle_search(const uint16_t *W, int64_t m, int64_t n, const float *h,
+                  int down, int up, float s_g, uint8_t *codes,
+                  uint8_t *packed, double *e_best, double *e_second,
+                  uint8_t *c0) {
+    return oracle_search_init(W, m, n, h, down, up, s_g, ORACLE_INIT_RTN, NULL,
+                              codes, packed, e_best, e_second, c0, NULL, NULL);
 }
 
 /* Quantize every group at a given scale code (the final re-quantization

@@ -46,13 +46,13 @@ def weights_f32(W_bits: np.ndarray) -> np.ndarray:
     return (np.asarray(W_bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
-def rtn_codes(W_bits: np.ndarray, s_g: float) -> np.ndarray:
-    """Max-abs initial code per group: fp32(max|w| / 6), fp32(. / s_g),
+def rtn_codes(W_bits: np.ndarray, s_g: float, anchor: float = 6.0) -> np.ndarray:
+    """Max-abs initial code per group: fp32(max|w| / anchor), fp32(. / s_g),
     torch's E4M3 cast, then at least code 1.  [m, n/16] int64."""
     w = weights_f32(W_bits)
     m, n = w.shape
     amax = np.abs(w).reshape(m, n // 16, 16).max(axis=-1).astype(np.float32)
-    s_init = (amax / np.float32(6.0)).astype(np.float32)
+    s_init = (amax / np.float32(anchor)).astype(np.float32)
     t = (s_init / np.float32(s_g)).astype(np.float32)
     return np.maximum(e4m3_cast_codes(t), 1)
 
@@ -109,3 +109,13 @@ def windowed_search(W_bits: np.ndarray, h, s_g: float, down: int, up: int):
             best_c = np.where(better, c, best_c)
     nib, _ = quantize_at(W_bits, s_g, best_c, h)
     return best_c, nib, best_e
+
+
+def four_over_six_codes(W_bits: np.ndarray, s_g: float) -> np.ndarray:
+    """4over6 initial code per group: the anchor (4 or 6) whose max-abs code
+    gives the smaller plain squared error, anchor 4 on a tie."""
+    c4 = rtn_codes(W_bits, s_g, 4.0)
+    c6 = rtn_codes(W_bits, s_g, 6.0)
+    _, l4 = quantize_at(W_bits, s_g, c4)
+    _, l6 = quantize_at(W_bits, s_g, c6)
+    return np.where(l4 <= l6, c4, c6)

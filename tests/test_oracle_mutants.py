@@ -27,8 +27,8 @@ MUTANTS = {
     "init_divides_by_4": ("double s_init = rn32(amax / 6.0);", "double s_init = rn32(amax / 4.0);"),
     "walk_clip_to_0": ("if (c < 1) c = 1;\n        if (c > ORACLE_M) c = ORACLE_M;\n        double e =",
                        "if (c < 0) c = 0;\n        if (c > ORACLE_M) c = ORACLE_M;\n        double e ="),
-    "h_slice_misindexed": ("hh[j] = (double)h[i * 16 + j];\n            double eb",
-                           "hh[j] = (double)h[(j * 16 + i) % n];\n            double eb"),
+    "h_slice_misindexed": ("hh[j] = (double)h[i * 16 + j];\n            int c0v;",
+                           "hh[j] = (double)h[(j * 16 + i) % n];\n            int c0v;"),
     "nibble_order_swapped": ("dst[k] = (uint8_t)(nib[2 * k] | (nib[2 * k + 1] << 4));",
                              "dst[k] = (uint8_t)(nib[2 * k + 1] | (nib[2 * k] << 4));"),
     "reciprocal_not_fp32": ("R[c] = (float)(1.0 / (double)S[c]);",
@@ -39,6 +39,14 @@ MUTANTS = {
     "hdiag_abs_not_square": ("h[j] += x * x;", "h[j] += fabs(x);"),
     "e4m3_subnormal_scale": ("if (e == 0) return (double)m / 8.0 * ldexp(1.0, -6);",
                              "if (e == 0) return (double)m / 8.0 * ldexp(1.0, -7);"),
+    "4over6_tie_to_anchor_6": ("return loss[0] <= loss[1] ? code[0] : code[1];",
+                               "return loss[0] < loss[1] ? code[0] : code[1];"),
+    "4over6_anchor_3": ("static const double anchors[2] = {4.0, 6.0};",
+                        "static const double anchors[2] = {3.0, 6.0};"),
+    "given_init_unclipped": ("c0v = init_codes[r * G + i];\n                if (c0v < 1) c0v = 1;",
+                             "c0v = init_codes[r * G + i];\n                if (c0v < 0) c0v = 1;"),
+    "accumulate_overwrites": ("            h[j] += x * x;\n        }\n    }\n}\n\n/* Loads group",
+                              "            h[j] = x * x;\n        }\n    }\n}\n\n/* Loads group"),
     "zero_drops_sign": ("if (nib) nib[j] = (uint8_t)((neg[j] << 3) | i);",
                         "if (nib) nib[j] = (uint8_t)(((neg[j] && i) << 3) | i);"),
 }
@@ -56,6 +64,7 @@ def test_pins_catch_planted_mistake(name, tmp_path):
                     "-o", str(lib), str(mutant), "-lm"], check=True)
     env = dict(os.environ, HSCALE_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", str(ROOT / "tests" / "test_oracle_pins.py"),
+                        str(ROOT / "tests" / "test_oracle_pins_init.py"),
                         "-q", "-x", "-p", "no:cacheprovider"],
                        capture_output=True, text=True, env=env, cwd=str(ROOT), timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
