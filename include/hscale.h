@@ -13,6 +13,12 @@
  *   hscale_quantize the final re-quantization at given scale codes (Sec. 3.3,
  *                   "Final re-quantization"; Eq. 12 at a fixed scale)
  *
+ * and the variants the paper's integration section and App. B use: the
+ * search from baseline-provided initial scales (HScaleGroupQuantize takes
+ * them as input), the 4over6 initialisation, a strided column-block form for
+ * GPTQ-style blockwise use, and h accumulated over streamed calibration
+ * batches.
+ *
  * Conventions shared by every entry point
  *   - All pointers are device pointers (hipMalloc'd or torch CUDA tensors)
  *     unless stated.  The caller allocates and owns every buffer; the library
@@ -65,6 +71,18 @@ typedef enum hscale_status {
     HSCALE_ERR_OVERLAP = -8    /* an output overlaps an input */
 } hscale_status;
 
+/* How the search chooses each group's initial code c0 before the walk. */
+typedef enum hscale_init_mode {
+    HSCALE_INIT_MAXABS = 0,  /* Eq. 7: fp32(max|w| / 6), fp32(. / s_g), Q_fp8 */
+    HSCALE_INIT_4OVER6 = 1,  /* App. B, 4over6 + H-Scale: anchors 4 and 6 as in
+                                Eq. 7 (fp32(max|w| / anchor)), each scored by
+                                the plain squared error sum_j (w_j - v_j S)^2
+                                at its code; the smaller wins, anchor 4 on a
+                                tie (scores in fp32, 4 chains of 4) */
+    HSCALE_INIT_GIVEN = 2    /* caller-provided code bytes; values outside
+                                1..126 are clipped into the ladder */
+} hscale_init_mode;
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *hscale_status_string(int status);
 
@@ -95,6 +113,23 @@ size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in);
  */
 int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
                  void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Streamed calibration (Eq. 4 over batches): h64[j] += sum_t X[t, j]^2 for
+ * one batch, into a caller-owned fp64 accumulator [in] (8-byte aligned) that
+ * the caller zeroes before the first batch.  Each batch's sum is formed
+ * exactly as in hscale_hdiag and added in fp64, so splitting the tokens into
+ * batches changes the result only at fp64 rounding level.  tokens == 0
+ * leaves h64 unchanged.  Other arguments as hscale_hdiag.
+ */
+int hscale_hdiag_accumulate(const void *X, int64_t tokens, int64_t in,
+                            double *h64, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+/* h[j] = fp32(h64[j]) (round to nearest even) for j < in; in % 16 == 0.
+ * Accumulating from zero and finalizing gives the same h as hscale_hdiag. */
+int hscale_hdiag_finalize(const double *h64, int64_t in, float *h,
+                          hipStream_t stream);
 
 /*
  * The per-group NVFP4 scale search of Sec. 3.3 (Eq. 7, 9-13) with the
@@ -131,6 +166,51 @@ int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h,
                      int32_t down, int32_t up, float global_scale,
                      uint8_t *scale_codes, uint8_t *packed_e2m1,
                      hipStream_t stream);
+
+/*
+ * The search with the 4over6 initial code (HSCALE_INIT_4OVER6); with
+ * down = up = 0 it is the 4over6 quantizer alone.  Arguments as
+ * hscale_search_du.
+ */
+int hscale_search_4over6(const void *W, int64_t out, int64_t in,
+                         const float *h, int32_t down, int32_t up,
+                         float global_scale, uint8_t *scale_codes,
+                         uint8_t *packed_e2m1, hipStream_t stream);
+
+/*
+ * The search from baseline-provided initial codes (HSCALE_INIT_GIVEN), the
+ * form of App. B's HScaleGroupQuantize: init_codes uint8 [out, in / 16], one
+ * E4M3FN code byte per group.  init_codes may equal scale_codes (refinement
+ * in place); any other overlap with an output is rejected.  Other arguments
+ * as hscale_search_du.
+ */
+int hscale_search_from(const void *W, int64_t out, int64_t in,
+                       const float *h, int32_t down, int32_t up,
+                       float global_scale, const uint8_t *init_codes,
+                       uint8_t *scale_codes, uint8_t *packed_e2m1,
+                       hipStream_t stream);
+
+/*
+ * The general strided form, for a column block of a larger matrix (App. B,
+ * the GPTQ combination searches W[:, i : i + B] with h[i : i + B] and the
+ * layer's fixed s_g).  W points at the block's first element; group (r, k)
+ * of the block is W[r * ldw + 16 k .. + 15].  h points at the block's h
+ * slice ([cols]).  Codes go to scale_codes[r * ldc + k], packed bytes to
+ * packed_e2m1[r * ldp + 8 k .. + 7]; init_codes[r * ldi + k] is read for
+ * HSCALE_INIT_GIVEN (may be NULL otherwise).
+ *
+ * cols % 16 == 0; ldw >= cols and ldw % 8 == 0 (16-byte rows); ldc >=
+ * cols / 16; ldp >= cols / 2 and ldp % 8 == 0; ldi >= cols / 16 when read.
+ * Alignment, window and global_scale rules as hscale_search.  Every other
+ * search entry point is this call with contiguous strides.
+ */
+int hscale_search_block(const void *W, int64_t ldw, int64_t out,
+                        int64_t cols, const float *h, int32_t down,
+                        int32_t up, float global_scale, int32_t init_mode,
+                        const uint8_t *init_codes, int64_t ldi,
+                        uint8_t *scale_codes, int64_t ldc,
+                        uint8_t *packed_e2m1, int64_t ldp,
+                        hipStream_t stream);
 
 /*
  * Final re-quantization at given scale codes (Sec. 3.3; Eq. 12 at a fixed

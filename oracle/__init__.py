@@ -75,6 +75,8 @@ def _load():
     lib.oracle_search_init.argtypes = [P, i64, i64, P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                        ctypes.c_int, P, P, P, P, P, P, P, P]
     lib.oracle_search_init.restype = ctypes.c_int
+    lib.oracle_anchor_codes.argtypes = [P, i64, i64, ctypes.c_float, ctypes.c_double, P]
+    lib.oracle_anchor_codes.restype = ctypes.c_int
     lib.oracle_hdiag_accumulate.argtypes = [P, i64, i64, P]
     lib.oracle_hdiag_accumulate.restype = None
     lib.oracle_quantize.argtypes = [P, i64, i64, ctypes.c_float, P, P, P, P]
@@ -196,6 +198,17 @@ def search(W, h, s_g: float, window: int | None = None, down: int | None = None,
     out = dict(codes=codes, packed=packed, e_best=e_best, e_second=e_second, c0=c0)
     if mode == INIT_4OVER6:
         out.update(l4=l4, l6=l6)
+    return out
+
+
+def anchor_codes(W, s_g: float, anchor: float) -> np.ndarray:
+    """Eq. 7's initial code with a general anchor (6: max-abs; 4 and 6: the
+    4over6 candidates).  [m, n/16] u8."""
+    W = _bf16_bits(W)
+    m, n = W.shape
+    out = np.zeros((m, n // 16), np.uint8)
+    if _load().oracle_anchor_codes(_ptr(W), m, n, np.float32(s_g), float(anchor), _ptr(out)) != 0:
+        raise ValueError("oracle_anchor_codes: bad arguments")
     return out
 
 

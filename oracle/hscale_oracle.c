@@ -362,6 +362,30 @@ int oracle_search(const uint16_t *W, int64_t m, int64_t n, const float *h,
                               codes, packed, e_best, e_second, c0, NULL, NULL);
 }
 
+/* Initial code of every group for a general anchor a (Eq. 7 has a = 6; the
+ * 4over6 initialisation compares a = 4 and a = 6):
+ * clip(Q_fp8(fp32(fp32(max|w| / a) / s_g)), 1, M).  out: [m, n/16]. */
+int oracle_anchor_codes(const uint16_t *W, int64_t m, int64_t n, float s_g,
+                        double anchor, uint8_t *out) {
+    if (n % 16 != 0 || !(s_g > 0.0f) || !(anchor > 0.0)) return -1;
+    int64_t G = n / 16;
+    double w[16];
+    int neg[16];
+    for (int64_t r = 0; r < m; ++r) {
+        for (int64_t i = 0; i < G; ++i) {
+            load_group(W, n, r, i, w, neg);
+            double amax = 0.0;
+            for (int j = 0; j < 16; ++j)
+                if (fabs(w[j]) > amax) amax = fabs(w[j]);
+            int c = oracle_e4m3_round(rn32(rn32(amax / anchor) / (double)s_g));
+            if (c < 1) c = 1;
+            if (c > ORACLE_M) c = ORACLE_M;
+            out[r * G + i] = (uint8_t)c;
+        }
+    }
+    return 0;
+}
+
 /* Quantize every group at a given scale code (the final re-quantization
  * step on its own).  err (optional) receives each group's Eq. 13 error
  * under h (h == NULL means h = 1). */

@@ -10,4 +10,5 @@ The compute is in ``libhscale.so`` (hand-written HIP, C ABI in
 ``include/hscale.h``); this package is its thin Python binding.
 """
 from ._lib import HScaleError, EXPORTS  # noqa: F401
-from .ops import hdiag, hdiag_workspace_bytes, quantize, search  # noqa: F401
+from .ops import (hdiag, hdiag_accumulate, hdiag_finalize, hdiag_workspace_bytes, quantize,  # noqa: F401
+                  search, search_block)

@@ -22,10 +22,17 @@ EXPORTS = (
     "hscale_status_string",
     "hscale_hdiag_workspace_bytes",
     "hscale_hdiag",
+    "hscale_hdiag_accumulate",
+    "hscale_hdiag_finalize",
     "hscale_search",
     "hscale_search_du",
+    "hscale_search_4over6",
+    "hscale_search_from",
+    "hscale_search_block",
     "hscale_quantize",
 )
+
+HSCALE_INIT_MAXABS, HSCALE_INIT_4OVER6, HSCALE_INIT_GIVEN = 0, 1, 2
 
 _lib = None
 
@@ -58,6 +65,16 @@ def load() -> ctypes.CDLL:
     lib.hscale_search_du.restype = ctypes.c_int
     lib.hscale_quantize.argtypes = [P, i64, i64, f32, P, P, P]
     lib.hscale_quantize.restype = ctypes.c_int
+    lib.hscale_hdiag_accumulate.argtypes = [P, i64, i64, P, P, sz, P]
+    lib.hscale_hdiag_accumulate.restype = ctypes.c_int
+    lib.hscale_hdiag_finalize.argtypes = [P, i64, P, P]
+    lib.hscale_hdiag_finalize.restype = ctypes.c_int
+    lib.hscale_search_4over6.argtypes = [P, i64, i64, P, i32, i32, f32, P, P, P]
+    lib.hscale_search_4over6.restype = ctypes.c_int
+    lib.hscale_search_from.argtypes = [P, i64, i64, P, i32, i32, f32, P, P, P, P]
+    lib.hscale_search_from.restype = ctypes.c_int
+    lib.hscale_search_block.argtypes = [P, i64, i64, i64, P, i32, i32, f32, i32, P, i64, P, i64, P, i64, P]
+    lib.hscale_search_block.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -92,3 +109,34 @@ def hscale_quantize(W: int, out: int, in_: int, global_scale: float, scale_codes
                     packed_e2m1: int, stream: int) -> int:
     return load().hscale_quantize(W or None, out, in_, global_scale, scale_codes or None,
                                   packed_e2m1 or None, stream or None)
+
+
+def hscale_hdiag_accumulate(X: int, tokens: int, in_: int, h64: int, workspace: int,
+                            workspace_bytes: int, stream: int) -> int:
+    return load().hscale_hdiag_accumulate(X or None, tokens, in_, h64 or None, workspace or None,
+                                          workspace_bytes, stream or None)
+
+
+def hscale_hdiag_finalize(h64: int, in_: int, h: int, stream: int) -> int:
+    return load().hscale_hdiag_finalize(h64 or None, in_, h or None, stream or None)
+
+
+def hscale_search_4over6(W: int, out: int, in_: int, h: int, down: int, up: int, global_scale: float,
+                         scale_codes: int, packed_e2m1: int, stream: int) -> int:
+    return load().hscale_search_4over6(W or None, out, in_, h or None, down, up, global_scale,
+                                       scale_codes or None, packed_e2m1 or None, stream or None)
+
+
+def hscale_search_from(W: int, out: int, in_: int, h: int, down: int, up: int, global_scale: float,
+                       init_codes: int, scale_codes: int, packed_e2m1: int, stream: int) -> int:
+    return load().hscale_search_from(W or None, out, in_, h or None, down, up, global_scale,
+                                     init_codes or None, scale_codes or None, packed_e2m1 or None,
+                                     stream or None)
+
+
+def hscale_search_block(W: int, ldw: int, out: int, cols: int, h: int, down: int, up: int,
+                        global_scale: float, init_mode: int, init_codes: int, ldi: int, scale_codes: int,
+                        ldc: int, packed_e2m1: int, ldp: int, stream: int) -> int:
+    return load().hscale_search_block(W or None, ldw, out, cols, h or None, down, up, global_scale,
+                                      init_mode, init_codes or None, ldi, scale_codes or None, ldc,
+                                      packed_e2m1 or None, ldp, stream or None)

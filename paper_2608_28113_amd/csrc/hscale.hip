@@ -165,9 +165,15 @@ __global__ __launch_bounds__(kHdThreads) void hdiag_partial(const u32x4 *__restr
 constexpr int kTreeCols = 64;
 constexpr int kTreeLanes = 4;
 
+// Sums the slice partials of each column in a fixed order: lane q of a
+// column adds slices q, q + 4, ...; the four lane sums combine as
+// ((s0 + s1) + s2) + s3.  kAccumulate adds the sum to an fp64 accumulator
+// instead of writing fp32 h.
+template <bool kAccumulate>
 __global__ __launch_bounds__(kTreeCols *kTreeLanes) void hdiag_tree(const double *__restrict__ partial,
                                                                      int64_t slices, int64_t in,
-                                                                     float *__restrict__ h) {
+                                                                     float *__restrict__ h,
+                                                                     double *__restrict__ h64) {
     const int lane = threadIdx.x % kTreeCols;
     const int q = threadIdx.x / kTreeCols;
     const int64_t col = (int64_t)blockIdx.x * kTreeCols + lane;
@@ -178,7 +184,19 @@ __global__ __launch_bounds__(kTreeCols *kTreeLanes) void hdiag_tree(const double
     __shared__ double red[kTreeLanes][kTreeCols];
     red[q][lane] = s;
     __syncthreads();
-    if (q == 0 && col < in) h[col] = (float)(((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]);
+    if (q == 0 && col < in) {
+        const double total = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+        if (kAccumulate)
+            h64[col] += total;
+        else
+            h[col] = (float)total;
+    }
+}
+
+__global__ __launch_bounds__(256) void hdiag_finalize_kernel(const double *__restrict__ h64, int64_t in,
+                                                             float *__restrict__ h) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j < in) h[j] = (float)h64[j];
 }
 
 // ---------------------------------------------------------------------------
@@ -295,17 +313,70 @@ __device__ __forceinline__ float group_error(const float (&w)[kGroup], const flo
 
 constexpr int kSearchThreads = 256;
 
-// Eq. 7 and 9-13 for one group held in registers: the max-abs initial code,
-// then the walk d = -down..up in pairs, keeping the first minimum.
+// How the walk's initial code c0 is chosen (values of the C ABI's init_mode).
+enum InitMode : int { kInitMaxAbs = 0, kInitFourOverSix = 1, kInitGiven = 2 };
+
+// Adds the squared residuals of elements 2K and 2K + 1 to the plain-error
+// chains (the 4over6 anchor score has no h).
+template <int K>
+__device__ __forceinline__ void accumulate_pair_plain(const float (&w)[kGroup], uint32_t src, float S,
+                                                      float (&e)[4]) {
+    const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, K & 3);
+    constexpr int j0 = 2 * K, j1 = 2 * K + 1;
+    const float r0 = fmaf(-v[0], S, w[j0]);
+    const float r1 = fmaf(-v[1], S, w[j1]);
+    e[j0 & 3] = fmaf(r0, r0, e[j0 & 3]);
+    e[j1 & 3] = fmaf(r1, r1, e[j1 & 3]);
+}
+
+// Plain squared error sum_j (w_j - v_j S)^2 of a packed group: single-rounding
+// residuals, 4 fp32 chains of 4.
+__device__ __forceinline__ float group_plain_error(const float (&w)[kGroup], uint2 p, float S) {
+    float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    accumulate_pair_plain<0>(w, p.x, S, e);
+    accumulate_pair_plain<1>(w, p.x, S, e);
+    accumulate_pair_plain<2>(w, p.x, S, e);
+    accumulate_pair_plain<3>(w, p.x, S, e);
+    accumulate_pair_plain<4>(w, p.y, S, e);
+    accumulate_pair_plain<5>(w, p.y, S, e);
+    accumulate_pair_plain<6>(w, p.y, S, e);
+    accumulate_pair_plain<7>(w, p.y, S, e);
+    return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+// Initial code of Eq. 7 from max|w| and an anchor (6 for max-abs; 4 or 6 for
+// 4over6): fp32(amax / anchor), then fp32(. / s_g), then Q_fp8 and the clip.
+__device__ __forceinline__ int anchor_code(float amax, float anchor, float s_g) {
+    const float s_init = amax / anchor;
+    return e4m3fn_code_clipped(s_init / s_g);
+}
+
+// Eq. 7 and 9-13 for one group held in registers: the initial code (by the
+// rule kInit; `given` is the caller's code for kInitGiven), then the walk
+// d = -down..up in pairs, keeping the first minimum.
+template <int kInit>
 __device__ __forceinline__ void search_group(const float (&w)[kGroup], const float (&hh)[kGroup],
-                                             const ScaleEntry *tab, int down, int up, float s_g, int &code,
-                                             uint2 &best_p) {
-    float amax = 0.0f;
+                                             const ScaleEntry *tab, int down, int up, float s_g, int given,
+                                             int &code, uint2 &best_p) {
+    int c0;
+    if (kInit == kInitGiven) {
+        c0 = min(max(given, 1), kMaxCode);
+    } else {
+        float amax = 0.0f;
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
-    const float s_init = amax / 6.0f;
-    const float t = s_init / s_g;
-    const int c0 = e4m3fn_code_clipped(t);
+        for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
+        c0 = anchor_code(amax, 6.0f, s_g);
+        if (kInit == kInitFourOverSix) {
+            // Anchor 4 (amax / 4 is exact) against anchor 6 by plain squared
+            // error; anchor 4 on a tie.
+            const int c4 = anchor_code(amax, 4.0f, s_g);
+            const ScaleEntry e4 = tab[c4 + kTabPad];
+            const ScaleEntry e6 = tab[c0 + kTabPad];
+            const float l4 = group_plain_error(w, quantize_group(w, e4.R, make_uint2(0u, 0u)), e4.S);
+            const float l6 = group_plain_error(w, quantize_group(w, e6.R, make_uint2(0u, 0u)), e6.S);
+            if (l4 <= l6) c0 = c4;
+        }
+    }
     const ScaleEntry *col = tab + (c0 + kTabPad);  // col[d] is candidate c0 + d, clipped
     float best_e = 0.0f;
     int best_d = -down;
@@ -345,48 +416,79 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
     code = min(max(c0 + best_d, 1), kMaxCode);
 }
 
-// One group per lane over the flat group index g = row * G + i (G = in / 16
-// groups per row), so a lane's h slice is h[16 i .. 16 i + 15].  A launch
-// normally covers every group once; larger problems loop with a grid stride.
-__global__ __launch_bounds__(kSearchThreads) void search_kernel(const u32x4 *__restrict__ W,
-                                                                const float4 *__restrict__ h,
-                                                                uint32_t num_groups, uint32_t G, int down,
-                                                                int up, float s_g, uint8_t *__restrict__ codes,
-                                                                uint2 *__restrict__ packed) {
+// Arguments of a search over a block of `rows` x (16 Gc) weights inside
+// larger row-major arrays.  Group (r, i) reads W at r * ldw + 16 i bf16
+// elements (ldw_vec counts 16-byte vectors), h at 16 i, the initial code at
+// r * ldi + i, and writes its code at r * ldc + i and its packed nibbles at
+// r * ldp + 8 i bytes (ldp_vec counts 8-byte words).
+struct SearchArgs {
+    const u32x4 *W;
+    uint64_t ldw_vec;
+    const float4 *h;
+    uint32_t num_groups;  // rows * Gc
+    uint32_t Gc;          // groups per row
+    int down, up;
+    float s_g;
+    const uint8_t *init;
+    uint64_t ldi;
+    uint8_t *codes;
+    uint64_t ldc;
+    uint2 *packed;
+    uint64_t ldp_vec;
+};
+
+// One group per lane over the flat index g = r * Gc + i of the block, so the
+// lanes of a wave cover consecutive groups of a row (contiguous loads and
+// stores) and a lane's h slice is h[16 i .. 16 i + 15].  A launch normally
+// covers every group once; larger problems loop with a grid stride.
+template <int kInit>
+__global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs a) {
     __shared__ ScaleEntry tab[kTabSize];
     __shared__ ScaleEntry uniq[kMaxCode + 1];
-    build_scale_table(tab, uniq, s_g);
+    build_scale_table(tab, uniq, a.s_g);
 
     const uint32_t stride = gridDim.x * kSearchThreads;
     const uint32_t first = blockIdx.x * kSearchThreads;  // wave-uniform
     uint32_t g = first + threadIdx.x;
-    if (g >= num_groups) return;
-    uint32_t i = first % G + threadIdx.x;  // column group of g
-    while (i >= G) i -= G;
-    const uint32_t step = stride % G;
+    if (g >= a.num_groups) return;
+    // (r, i) of g from the uniform block offset: at most one wrap per row
+    // crossed inside the block.
+    uint32_t r = first / a.Gc;
+    uint32_t i = first % a.Gc + threadIdx.x;
+    while (i >= a.Gc) {
+        i -= a.Gc;
+        ++r;
+    }
+    const uint32_t step_r = stride / a.Gc, step_i = stride % a.Gc;
 
     for (;;) {
         float w[kGroup];
-        load_group(W, g, w);
+        const u32x4 *src = a.W + (uint64_t)r * a.ldw_vec + 2 * (uint64_t)i;
+        load_group(src, 0, w);
         float hh[kGroup];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float4 v = h[4 * i + q];
+            const float4 v = a.h[4 * (uint64_t)i + q];
             hh[4 * q] = v.x;
             hh[4 * q + 1] = v.y;
             hh[4 * q + 2] = v.z;
             hh[4 * q + 3] = v.w;
         }
+        const int given = kInit == kInitGiven ? (int)a.init[(uint64_t)r * a.ldi + i] : 0;
         int code;
         uint2 best_p;
-        search_group(w, hh, tab, down, up, s_g, code, best_p);
-        codes[g] = (uint8_t)code;
-        packed[g] = best_p;
+        search_group<kInit>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p);
+        a.codes[(uint64_t)r * a.ldc + i] = (uint8_t)code;
+        a.packed[(uint64_t)r * a.ldp_vec + i] = best_p;
 
-        if (num_groups - g <= stride) break;
+        if (a.num_groups - g <= stride) break;
         g += stride;
-        i += step;
-        if (i >= G) i -= G;
+        r += step_r;
+        i += step_i;
+        if (i >= a.Gc) {
+            i -= a.Gc;
+            ++r;
+        }
     }
 }
 
@@ -442,21 +544,101 @@ int grid_for(int64_t groups) {
 
 int launch_status() { return hipGetLastError() == hipSuccess ? HSCALE_OK : HSCALE_ERR_HIP; }
 
-int check_search_args(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
-                      float s_g, const uint8_t *codes, const uint8_t *packed) {
-    if (out < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
-    if (out > 0 && in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+// Bytes spanned by `rows` rows of `width` elements at a row stride of `ld`
+// elements of `elem` bytes each.
+size_t span(int64_t rows, int64_t ld, int64_t width, size_t elem) {
+    if (rows <= 0 || width <= 0) return 0;
+    return ((size_t)(rows - 1) * (size_t)ld + (size_t)width) * elem;
+}
+
+int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
+                 float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, uint8_t *codes, int64_t ldc,
+                 uint8_t *packed, int64_t ldp, hipStream_t stream) {
+    if (out < 0 || cols < 0 || cols % kGroup != 0) return HSCALE_ERR_SHAPE;
+    const int64_t Gc = cols / kGroup;
+    if (out > 0 && cols > 0 && out > kMaxGroups / Gc) return HSCALE_ERR_SHAPE;
+    if (init_mode < kInitMaxAbs || init_mode > kInitGiven) return HSCALE_ERR_SHAPE;
     if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
     if (!scale_ok(s_g)) return HSCALE_ERR_SCALE;
-    if (out == 0 || in == 0) return HSCALE_OK;
-    if (!W || !h || !codes || !packed) return HSCALE_ERR_NULL;
-    if (!aligned(W, 16) || !aligned(h, 16) || !aligned(packed, 8)) return HSCALE_ERR_ALIGN;
-    const size_t nw = (size_t)out * (size_t)in * 2, nh = (size_t)in * 4;
-    const size_t nc = (size_t)out * (size_t)(in / kGroup), np = (size_t)out * (size_t)(in / 2);
+    if (out == 0 || cols == 0) return HSCALE_OK;
+    if (ldw < cols || ldc < Gc || ldp < cols / 2 || (init_mode == kInitGiven && ldi < Gc)) return HSCALE_ERR_SHAPE;
+    if (!W || !h || !codes || !packed || (init_mode == kInitGiven && !init_codes)) return HSCALE_ERR_NULL;
+    if (!aligned(W, 16) || ldw % 8 != 0 || !aligned(h, 16) || !aligned(packed, 8) || ldp % 8 != 0)
+        return HSCALE_ERR_ALIGN;
+    const size_t nw = span(out, ldw, cols, 2), nh = (size_t)cols * 4;
+    const size_t nc = span(out, ldc, Gc, 1), np = span(out, ldp, cols / 2, 1);
     if (overlaps(codes, nc, W, nw) || overlaps(codes, nc, h, nh) || overlaps(packed, np, W, nw) ||
         overlaps(packed, np, h, nh) || overlaps(codes, nc, packed, np))
         return HSCALE_ERR_OVERLAP;
-    return HSCALE_OK;
+    if (init_mode == kInitGiven) {
+        // The codes may be refined in place (init_codes == scale_codes with
+        // the same stride: each group reads its own byte before writing it).
+        const size_t ni = span(out, ldi, Gc, 1);
+        const bool in_place = init_codes == codes && ldi == ldc;
+        if ((!in_place && overlaps(init_codes, ni, codes, nc)) || overlaps(init_codes, ni, packed, np))
+            return HSCALE_ERR_OVERLAP;
+    }
+    SearchArgs a;
+    a.W = static_cast<const u32x4 *>(W);
+    a.ldw_vec = (uint64_t)ldw / 8;
+    a.h = reinterpret_cast<const float4 *>(h);
+    a.num_groups = (uint32_t)(out * Gc);
+    a.Gc = (uint32_t)Gc;
+    a.down = down;
+    a.up = up;
+    a.s_g = s_g;
+    a.init = init_codes;
+    a.ldi = (uint64_t)ldi;
+    a.codes = codes;
+    a.ldc = (uint64_t)ldc;
+    a.packed = reinterpret_cast<uint2 *>(packed);
+    a.ldp_vec = (uint64_t)ldp / 8;
+    const dim3 grid(grid_for(out * Gc)), block(kSearchThreads);
+    switch (init_mode) {
+        case kInitMaxAbs: hipLaunchKernelGGL(search_kernel<kInitMaxAbs>, grid, block, 0, stream, a); break;
+        case kInitFourOverSix: hipLaunchKernelGGL(search_kernel<kInitFourOverSix>, grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL(search_kernel<kInitGiven>, grid, block, 0, stream, a); break;
+    }
+    return launch_status();
+}
+
+int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, void *workspace,
+              size_t workspace_bytes, hipStream_t stream) {
+    if (tokens < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    if (in == 0) return HSCALE_OK;
+    const bool accumulate = h64 != nullptr;
+    if (!accumulate && !h) return HSCALE_ERR_NULL;
+    if (!accumulate && !aligned(h, 4)) return HSCALE_ERR_ALIGN;
+    if (accumulate && !aligned(h64, 8)) return HSCALE_ERR_ALIGN;
+    const HdiagPlan p = hdiag_plan(tokens, in);
+    const size_t need = hscale_hdiag_workspace_bytes(tokens, in);
+    const size_t nout = accumulate ? (size_t)in * 8 : (size_t)in * 4;
+    const void *out = accumulate ? (const void *)h64 : (const void *)h;
+    if (tokens > 0) {
+        if (!X) return HSCALE_ERR_NULL;
+        if (!aligned(X, 16)) return HSCALE_ERR_ALIGN;
+        if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
+        if (!workspace) return HSCALE_ERR_NULL;
+        if (!aligned(workspace, 16)) return HSCALE_ERR_ALIGN;
+        const size_t nx = (size_t)tokens * (size_t)in * 2;
+        if (overlaps(out, nout, X, nx) || overlaps(workspace, need, X, nx) || overlaps(workspace, need, out, nout))
+            return HSCALE_ERR_OVERLAP;
+        dim3 grid((unsigned)p.tiles, (unsigned)p.slices);
+        hipLaunchKernelGGL(hdiag_partial, grid, dim3(kHdThreads), 0, stream, static_cast<const u32x4 *>(X),
+                           tokens, in, p.slice_tokens, static_cast<double *>(workspace));
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    } else if (accumulate) {
+        return HSCALE_OK;  // nothing to add
+    }
+    const unsigned tree_blocks = (unsigned)((in + kTreeCols - 1) / kTreeCols);
+    if (accumulate)
+        hipLaunchKernelGGL(hdiag_tree<true>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
+                           static_cast<const double *>(workspace), p.slices, in, (float *)nullptr, h64);
+    else
+        hipLaunchKernelGGL(hdiag_tree<false>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
+                           static_cast<const double *>(workspace), p.slices, in, h, (double *)nullptr);
+    return launch_status();
 }
 
 }  // namespace
@@ -486,50 +668,54 @@ size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in) {
 
 int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h, void *workspace, size_t workspace_bytes,
                  hipStream_t stream) {
-    if (tokens < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
-    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    return hdiag_run(X, tokens, in, h, nullptr, workspace, workspace_bytes, stream);
+}
+
+int hscale_hdiag_accumulate(const void *X, int64_t tokens, int64_t in, double *h64, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+    if (in > 0 && !h64) return HSCALE_ERR_NULL;
+    return hdiag_run(X, tokens, in, nullptr, h64, workspace, workspace_bytes, stream);
+}
+
+int hscale_hdiag_finalize(const double *h64, int64_t in, float *h, hipStream_t stream) {
+    if (in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
     if (in == 0) return HSCALE_OK;
-    if (!h) return HSCALE_ERR_NULL;
-    if (!aligned(h, 4)) return HSCALE_ERR_ALIGN;
-    const HdiagPlan p = hdiag_plan(tokens, in);
-    const size_t need = hscale_hdiag_workspace_bytes(tokens, in);
-    if (tokens > 0) {
-        if (!X) return HSCALE_ERR_NULL;
-        if (!aligned(X, 16)) return HSCALE_ERR_ALIGN;
-        if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
-        if (!workspace) return HSCALE_ERR_NULL;
-        if (!aligned(workspace, 16)) return HSCALE_ERR_ALIGN;
-        const size_t nx = (size_t)tokens * (size_t)in * 2;
-        if (overlaps(h, (size_t)in * 4, X, nx) || overlaps(workspace, need, X, nx) ||
-            overlaps(workspace, need, h, (size_t)in * 4))
-            return HSCALE_ERR_OVERLAP;
-        dim3 grid((unsigned)p.tiles, (unsigned)p.slices);
-        hipLaunchKernelGGL(hdiag_partial, grid, dim3(kHdThreads), 0, stream, static_cast<const u32x4 *>(X),
-                           tokens, in, p.slice_tokens, static_cast<double *>(workspace));
-        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
-    }
-    const unsigned tree_blocks = (unsigned)((in + kTreeCols - 1) / kTreeCols);
-    hipLaunchKernelGGL(hdiag_tree, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
-                       static_cast<const double *>(workspace), p.slices, in, h);
+    if (!h64 || !h) return HSCALE_ERR_NULL;
+    if (!aligned(h64, 8) || !aligned(h, 4)) return HSCALE_ERR_ALIGN;
+    if (overlaps(h64, (size_t)in * 8, h, (size_t)in * 4)) return HSCALE_ERR_OVERLAP;
+    hipLaunchKernelGGL(hdiag_finalize_kernel, dim3((unsigned)((in + 255) / 256)), dim3(256), 0, stream, h64, in, h);
     return launch_status();
+}
+
+int hscale_search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down,
+                        int32_t up, float global_scale, int32_t init_mode, const uint8_t *init_codes, int64_t ldi,
+                        uint8_t *scale_codes, int64_t ldc, uint8_t *packed_e2m1, int64_t ldp, hipStream_t stream) {
+    return search_block(W, ldw, out, cols, h, down, up, global_scale, init_mode, init_codes, ldi, scale_codes, ldc,
+                        packed_e2m1, ldp, stream);
 }
 
 int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
                      float global_scale, uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
-    const int st = check_search_args(W, out, in, h, down, up, global_scale, scale_codes, packed_e2m1);
-    if (st != HSCALE_OK || out == 0 || in == 0) return st;
-    const int64_t G = in / kGroup;
-    const int64_t groups = out * G;
-    hipLaunchKernelGGL(search_kernel, dim3(grid_for(groups)), dim3(kSearchThreads), 0, stream,
-                       static_cast<const u32x4 *>(W), reinterpret_cast<const float4 *>(h), (uint32_t)groups,
-                       (uint32_t)G, (int)down, (int)up, global_scale, scale_codes,
-                       reinterpret_cast<uint2 *>(packed_e2m1));
-    return launch_status();
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitMaxAbs, nullptr, 0, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream);
 }
 
 int hscale_search(const void *W, int64_t out, int64_t in, const float *h, int32_t window, float global_scale,
                   uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
     return hscale_search_du(W, out, in, h, window, window, global_scale, scale_codes, packed_e2m1, stream);
+}
+
+int hscale_search_4over6(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                         float global_scale, uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitFourOverSix, nullptr, 0, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream);
+}
+
+int hscale_search_from(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                       float global_scale, const uint8_t *init_codes, uint8_t *scale_codes, uint8_t *packed_e2m1,
+                       hipStream_t stream) {
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitGiven, init_codes, in / kGroup,
+                        scale_codes, in / kGroup, packed_e2m1, in / 2, stream);
 }
 
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,

@@ -50,32 +50,120 @@ def hdiag(X: torch.Tensor, h: torch.Tensor | None = None, workspace: torch.Tenso
     return h
 
 
+def _init_mode(init):
+    if isinstance(init, str):
+        return {"maxabs": _lib.HSCALE_INIT_MAXABS, "rtn": _lib.HSCALE_INIT_MAXABS,
+                "4over6": _lib.HSCALE_INIT_4OVER6}[init], None
+    if isinstance(init, torch.Tensor):
+        if init.dtype != torch.uint8 or not init.is_cuda:
+            raise ValueError("initial codes must be a uint8 CUDA tensor")
+        return _lib.HSCALE_INIT_GIVEN, init
+    raise ValueError("init must be 'maxabs', '4over6' or a uint8 tensor of codes")
+
+
 def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | None = None,
-           down: int | None = None, up: int | None = None, scale_codes: torch.Tensor | None = None,
-           packed_e2m1: torch.Tensor | None = None, stream=None):
+           down: int | None = None, up: int | None = None, init="maxabs",
+           scale_codes: torch.Tensor | None = None, packed_e2m1: torch.Tensor | None = None, stream=None):
     """The per-group NVFP4 scale search (Sec. 3.3).  Returns
-    (scale_codes uint8 [out, in/16], packed_e2m1 uint8 [out, in/2])."""
+    (scale_codes uint8 [out, in/16], packed_e2m1 uint8 [out, in/2]).
+
+    ``window`` gives the symmetric shift set -window..+window; ``down``/``up``
+    the paper's asymmetric one.  ``init`` is "maxabs" (Eq. 7), "4over6", or a
+    uint8 tensor [out, in/16] of initial codes (it may be ``scale_codes``
+    itself, to refine in place).
+    """
     _bf16_matrix(W, "W")
     m, n = W.shape
     if h.dtype != torch.float32 or h.shape != (n,) or not h.is_contiguous():
         raise ValueError("h must be a contiguous fp32 tensor of shape [in]")
+    if window is not None:
+        if down is not None or up is not None:
+            raise ValueError("give either window or down/up")
+        down = up = int(window)
+    if down is None or up is None:
+        raise ValueError("give window or both down and up")
+    mode, init_t = _init_mode(init)
     if scale_codes is None:
         scale_codes = torch.empty((m, n // 16), dtype=torch.uint8, device=W.device)
     if packed_e2m1 is None:
         packed_e2m1 = torch.empty((m, n // 2), dtype=torch.uint8, device=W.device)
     s = _stream(stream)
-    if window is not None:
-        if down is not None or up is not None:
-            raise ValueError("give either window or down/up")
-        st = _lib.hscale_search(W.data_ptr(), m, n, h.data_ptr(), int(window), float(global_scale),
-                                scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
-        _check(st, "hscale_search")
-    else:
-        st = _lib.hscale_search_du(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up),
-                                   float(global_scale), scale_codes.data_ptr(),
-                                   packed_e2m1.data_ptr(), s)
+    if mode == _lib.HSCALE_INIT_MAXABS:
+        st = _lib.hscale_search_du(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale),
+                                   scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_du")
+    elif mode == _lib.HSCALE_INIT_4OVER6:
+        st = _lib.hscale_search_4over6(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up),
+                                       float(global_scale), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        _check(st, "hscale_search_4over6")
+    else:
+        if init_t.shape != (m, n // 16) or not init_t.is_contiguous():
+            raise ValueError("initial codes must be a contiguous uint8 tensor [out, in/16]")
+        st = _lib.hscale_search_from(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale),
+                                     init_t.data_ptr(), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        _check(st, "hscale_search_from")
     return scale_codes, packed_e2m1
+
+
+def _row_view(t: torch.Tensor, dtype, name: str):
+    if t.dtype != dtype or t.dim() != 2 or not t.is_cuda or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name} must be a 2-D {dtype} CUDA tensor (view) with unit column stride")
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
+def search_block(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: int, up: int,
+                 scale_codes: torch.Tensor, packed_e2m1: torch.Tensor, init="maxabs", stream=None):
+    """The search on a column block given as strided views: W = Wfull[:, a:b]
+    (bf16), h = hfull[a:b], scale_codes = codes[:, a/16:b/16] and
+    packed_e2m1 = packed[:, a/2:b/2] (uint8), as in the paper's GPTQ
+    combination (App. B).  Outputs are written in place."""
+    m, cols = W.shape
+    ldw = _row_view(W, torch.bfloat16, "W")
+    ldc = _row_view(scale_codes, torch.uint8, "scale_codes")
+    ldp = _row_view(packed_e2m1, torch.uint8, "packed_e2m1")
+    if scale_codes.shape != (m, cols // 16) or packed_e2m1.shape != (m, cols // 2):
+        raise ValueError("output views do not match the block")
+    if h.dtype != torch.float32 or h.shape != (cols,) or not h.is_contiguous():
+        raise ValueError("h must be a contiguous fp32 slice of shape [cols]")
+    mode, init_t = _init_mode(init)
+    ldi = 0
+    iptr = 0
+    if init_t is not None:
+        ldi = _row_view(init_t, torch.uint8, "init codes")
+        if init_t.shape != (m, cols // 16):
+            raise ValueError("initial codes do not match the block")
+        iptr = init_t.data_ptr()
+    st = _lib.hscale_search_block(W.data_ptr(), ldw, m, cols, h.data_ptr(), int(down), int(up),
+                                  float(global_scale), mode, iptr, ldi, scale_codes.data_ptr(), ldc,
+                                  packed_e2m1.data_ptr(), ldp, _stream(stream))
+    _check(st, "hscale_search_block")
+    return scale_codes, packed_e2m1
+
+
+def hdiag_accumulate(X: torch.Tensor, h64: torch.Tensor, workspace: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+    """h64 += diag(X^T X) for one calibration batch (fp64 accumulator)."""
+    _bf16_matrix(X, "X")
+    T, n = X.shape
+    if h64.dtype != torch.float64 or h64.shape != (n,) or not h64.is_contiguous():
+        raise ValueError("h64 must be a contiguous fp64 tensor of shape [in]")
+    need = hdiag_workspace_bytes(T, n)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.hscale_hdiag_accumulate(X.data_ptr(), T, n, h64.data_ptr(), ws_ptr, ws_bytes,
+                                        _stream(stream)), "hscale_hdiag_accumulate")
+    return h64
+
+
+def hdiag_finalize(h64: torch.Tensor, h: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """h = fp32(h64)."""
+    n = h64.shape[0]
+    if h is None:
+        h = torch.empty(n, dtype=torch.float32, device=h64.device)
+    _check(_lib.hscale_hdiag_finalize(h64.data_ptr(), n, h.data_ptr(), _stream(stream)), "hscale_hdiag_finalize")
+    return h
 
 
 def quantize(W: torch.Tensor, global_scale: float, scale_codes: torch.Tensor,

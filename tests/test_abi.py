@@ -132,3 +132,41 @@ def test_torch_front_end_rejects_bad_tensors():
         ops.hdiag(torch.zeros(4, 16, dtype=torch.float32))
     with pytest.raises(ValueError):
         ops.search(torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(16), 1e-3, window=4)
+
+
+def test_variant_validation(L):
+    m, n = 4, 64
+    W, h, codes, packed, init, h64 = A, 2 * A, 3 * A, 4 * A, 5 * A, 6 * A
+    # Every call here must fail validation (or be empty) so that nothing is
+    # launched: the addresses are fake.  4over6 and given-init share the
+    # search validation.
+    assert L.hscale_search_4over6(W, m, n, h, 9, 126, 1e-3, codes, packed, 0) == -4
+    assert L.hscale_search_4over6(W, m, 17, h, 9, 6, 1e-3, codes, packed, 0) == -2
+    assert L.hscale_search_from(W, m, n, h, 4, 4, 1e-3, 0, codes, packed, 0) == -1
+    assert L.hscale_search_from(W, m, n, h, 4, 4, 1e-3, codes + 1, codes, packed, 0) == -8  # partial overlap
+    assert L.hscale_search_from(W, m, n, h, 4, 4, 0.0, init, codes, packed, 0) == -5
+    # strided block
+    blk = lambda **k: L.hscale_search_block(k.get("W", W), k.get("ldw", 128), k.get("out", m), k.get("cols", n),
+                                            h, 4, 4, 1e-3, k.get("mode", 0), k.get("init", 0), k.get("ldi", 0),
+                                            codes, k.get("ldc", 8), packed, k.get("ldp", 64), 0)
+    assert blk(cols=48 + 8) == -2
+    assert blk(ldw=32) == -2            # ldw < cols
+    assert blk(ldw=68) == -3            # rows not 16-byte aligned
+    assert blk(ldc=3) == -2
+    assert blk(ldp=31) == -2
+    assert blk(ldp=36) == -3            # packed rows not 8-byte aligned
+    assert blk(mode=3) == -2
+    assert blk(mode=2, ldi=4) == -1     # given init without codes
+    assert blk(mode=2, init=init, ldi=2) == -2
+    assert blk(out=0) == 0
+    # accumulate / finalize
+    ws = L.hscale_hdiag_workspace_bytes(64, 32)
+    assert L.hscale_hdiag_accumulate(A, 64, 32, 0, 3 * A, ws, 0) == -1
+    assert L.hscale_hdiag_accumulate(A, 64, 32, h64 + 4, 3 * A, ws, 0) == -3
+    assert L.hscale_hdiag_accumulate(A, 64, 33, h64, 3 * A, ws, 0) == -2
+    assert L.hscale_hdiag_accumulate(A, 64, 32, A + 8, 3 * A, ws, 0) == -8
+    assert L.hscale_hdiag_accumulate(0, 0, 32, h64, 0, 0, 0) == 0  # empty batch: no-op, no launch
+    assert L.hscale_hdiag_finalize(0, 32, h, 0) == -1
+    assert L.hscale_hdiag_finalize(h64, 33, h, 0) == -2
+    assert L.hscale_hdiag_finalize(h64, 32, h64 + 64, 0) == -8
+    assert L.hscale_hdiag_finalize(0, 0, 0, 0) == 0

@@ -128,3 +128,10 @@ def test_4over6_tie_goes_to_anchor_4():
     assert r["l4"][0, 0] == 0.0 and r["l6"][0, 0] == 0.0
     assert r["codes"][0, 0] == 60
     assert libref.four_over_six_codes(Wb, s_g)[0, 0] == 60
+
+
+def test_anchor_codes():
+    Wb, h, s_g = _tiny_inputs()
+    assert np.array_equal(oracle.anchor_codes(Wb, s_g, 6.0), libref.rtn_codes(Wb, s_g, 6.0))
+    assert np.array_equal(oracle.anchor_codes(Wb, s_g, 4.0), libref.rtn_codes(Wb, s_g, 4.0))
+    assert np.array_equal(oracle.anchor_codes(Wb, s_g, 6.0), oracle.search(Wb, h, s_g, window=0)["c0"])
