@@ -1,28 +1,34 @@
 #!/usr/bin/env python3
 """Benchmark of the H-Scale hot path on one MI355X.
 
-One step = one pass of the whole path over one linear layer:
-  hdiag  (h = diag(X^T X) from the calibration activations X), then
-  search (the +-window E4M3 scale search of every 16-weight group of W,
-          scored with that h, writing scale codes and packed E2M1 codes).
+One step = one pass of the whole path over one workload:
+  hdiag  (h = diag(X^T X)) over each calibration activation tensor, then
+  search (the E4M3 scale search of every 16-weight group of each weight
+          matrix, scored with its input's h, writing scale codes and packed
+          E2M1 codes).
 Inputs are resident in HBM before the timed region starts.  The default
 workload is the Llama-3-8B-shaped MLP down_proj: W 4096 x 14336 bf16 and
-X 262144 x 14336 bf16 (128 sequences x 2048 tokens), window +-4.
+X 262144 x 14336 bf16 (128 sequences x 2048 tokens), window +-4.  Other
+workloads: attn_proj (4096 x 4096), down_proj_70b (8192 x 28672, +-8) and
+block (an 8B-class decoder block: q/k/v/o and gate/up/down with three shared
+activation tensors of 262144 tokens).
 
 Timing: W untimed warm-up steps, then K timed steps bracketed by device
-synchronisation; each kernel call is bracketed by HIP events recorded on
-the stream the library launches on (torch's current stream, passed through
-the C ABI).  The 7.5 GB read of X in each step evicts W from the 256 MB
-Infinity Cache, so the search reads W from HBM.
+synchronisation; each kernel call is bracketed by HIP events recorded on the
+stream the library launches on (torch's current stream, passed through the C
+ABI).  The multi-GB reads of X in each step evict W from the 256 MB Infinity
+Cache, so the search reads W from HBM.
 
 Prints one JSON line.  `value` is the search throughput in Gweights/s (the
 metric's first figure); `hdiag` carries the second figure (HBM GB/s and its
 fraction of the 8 TB/s peak).  `cpu_baseline` is the CPU oracle timed on a
-bounded sample of the same workload on this host.
+bounded sample of the same workload on this host; the same sample is checked
+for parity against the benchmarked outputs.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -36,28 +42,30 @@ HBM_PEAK_GBS = 8000.0
 # op per 2 clocks) x 2.4 GHz = 78.64 T lane-ops/s = 157.3 TFLOP/s of FMA.
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
 SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
+HERE = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SRC = os.path.join(HERE, "paper_2608_28113_amd", "csrc", "hscale.hip")
 
 
-def search_ops_per_weight(K: int) -> int:
+def search_ops_per_weight(K: int, init: str) -> int:
     # 5 per weight-candidate (scale product, grid rounding, residual,
-    # square, weighted accumulate) + 3 per weight (max, encode, pack).
-    return 5 * K + 3
+    # square, weighted accumulate) + 3 per weight (max, encode, pack); the
+    # 4over6 initial code adds two anchor evaluations of 4 ops per weight
+    # (scale product, rounding, residual, square-accumulate).
+    return 5 * K + 3 + (8 if init == "4over6" else 0)
 
 
-PROFILE_JSON = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                            "down_proj_4096x14336_t262144_w4.json")
-KERNEL_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_28113_amd", "csrc",
-                          "hscale.hip")
+def profile_json(workload: str) -> str:
+    return os.path.join(HERE, "profiles", f"{workload}.json")
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary (copy-calibrated), or None when that summary was taken on another
-    workload or before the kernels last changed."""
-    import hashlib
-    if workload != "down_proj" or not os.path.exists(PROFILE_JSON):
+    """HBM bytes per step from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary of this workload (copy-calibrated), or None when there is none or
+    it was taken before the kernels last changed."""
+    path = profile_json(workload)
+    if not os.path.exists(path):
         return None
-    with open(PROFILE_JSON) as f:
+    with open(path) as f:
         prof = json.load(f)
     with open(KERNEL_SRC, "rb") as f:
         src = hashlib.sha256(f.read()).hexdigest()[:16]
@@ -69,7 +77,8 @@ def measured_traffic(workload: str):
         if not all(n in t for n in names):
             return None
         return sum(t[n]["read_bytes"] + t[n]["write_bytes"] for n in names)
-    return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot("search_kernel")}
+    return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot("search_kernel"),
+            "source": os.path.relpath(path, HERE)}
 
 
 def parse():
@@ -77,8 +86,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="down_proj")
-    ap.add_argument("--window", type=int, default=None)
+    ap.add_argument("--workload", default="down_proj",
+                    choices=["tiny", "attn_proj", "down_proj", "down_proj_70b", "block"])
+    ap.add_argument("--window", type=int, default=None, help="symmetric shift set -w..+w")
+    ap.add_argument("--down", type=int, default=None, help="asymmetric shift set -down..+up")
+    ap.add_argument("--up", type=int, default=None)
+    ap.add_argument("--init", default="maxabs", choices=["maxabs", "4over6"])
     ap.add_argument("--cpu-rows", type=int, default=1024,
                     help="rows of W in the CPU oracle sample (also checked for parity)")
     ap.add_argument("--cpu-tokens", type=int, default=32768,
@@ -92,6 +105,30 @@ def parse():
     return ap.parse_args()
 
 
+def build_workload(name, dev, window_override):
+    """Returns (activations {key: X}, layers [(label, W, x_key, s_g, window)], description)."""
+    from synth.workloads import CONFIGS, block_workloads, harness_global_scale, make_activations, make_weight
+    if name != "block":
+        wl = CONFIGS[name]
+        w = wl.window if window_override is None else window_override
+        X = make_activations(wl, dev)
+        W = make_weight(wl, dev)
+        desc = f"{wl.name}: W {wl.out}x{wl.inp} bf16 ({wl.w_dist}), X {wl.tokens}x{wl.inp} bf16"
+        return {"x": X}, [(wl.name, W, "x", harness_global_scale(W), w)], desc
+    wls = block_workloads(window=4 if window_override is None else window_override)
+    xkey = {"q_proj": "attn", "k_proj": "attn", "v_proj": "attn", "o_proj": "attn",
+            "gate_proj": "mlp", "up_proj": "mlp", "down_proj": "down"}
+    acts = {"attn": make_activations(wls["q_proj"], dev), "mlp": make_activations(wls["gate_proj"], dev),
+            "down": make_activations(wls["down_proj"], dev)}
+    layers = []
+    for lname, wl in wls.items():
+        W = make_weight(wl, dev)
+        layers.append((lname, W, xkey[lname], harness_global_scale(W), wl.window))
+    desc = ("8B-class decoder block: q/o 4096x4096, k/v 1024x4096, gate/up 14336x4096, down 4096x14336 bf16; "
+            "X_attn and X_mlp 262144x4096, X_down 262144x14336 bf16")
+    return acts, layers, desc
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -100,49 +137,57 @@ def main():
               "communication (rows shard with no exchange; see the sharding notes). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if (args.down is None) != (args.up is None) or (args.window is not None and args.down is not None):
+        print("give --window, or both --down and --up", file=sys.stderr)
+        sys.exit(2)
 
     import torch
     import paper_2608_28113_amd as hs
     from paper_2608_28113_amd import _lib
-    from synth.workloads import CONFIGS, harness_global_scale, make_activations, make_weight, tensor_bits
 
     _lib.load()
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
-    wl = CONFIGS[args.workload]
-    window = wl.window if args.window is None else args.window
-    K = 2 * window + 1
     dev = "cuda"
     torch.cuda.set_device(0)
 
-    X = make_activations(wl, dev)
-    W = make_weight(wl, dev)
-    s_g = harness_global_scale(W)
-    m, n, T = wl.out, wl.inp, wl.tokens
-    h = torch.empty(n, dtype=torch.float32, device=dev)
-    ws = torch.empty(max(hs.hdiag_workspace_bytes(T, n), 16), dtype=torch.uint8, device=dev)
-    codes = torch.empty((m, n // 16), dtype=torch.uint8, device=dev)
-    packed = torch.empty((m, n // 2), dtype=torch.uint8, device=dev)
+    acts, layers, desc = build_workload(args.workload, dev, args.window)
+    if args.down is not None:
+        layers = [(l, W, xk, s, None) for (l, W, xk, s, _) in layers]
+    hbuf = {k: torch.empty(X.shape[1], dtype=torch.float32, device=dev) for k, X in acts.items()}
+    ws = torch.empty(max(max(hs.hdiag_workspace_bytes(*X.shape) for X in acts.values()), 16),
+                     dtype=torch.uint8, device=dev)
+    outs = [(torch.empty((W.shape[0], W.shape[1] // 16), dtype=torch.uint8, device=dev),
+             torch.empty((W.shape[0], W.shape[1] // 2), dtype=torch.uint8, device=dev)) for (_, W, _, _, _) in layers]
     torch.cuda.synchronize()
-
     stream = torch.cuda.current_stream()
 
-    def step(evs=None):
-        if evs is not None:
-            evs[0].record(stream)
-        hs.hdiag(X, h=h, workspace=ws, stream=stream)
-        if evs is not None:
-            evs[1].record(stream)
-        hs.search(W, h, s_g, window=window, scale_codes=codes, packed_e2m1=packed, stream=stream)
-        if evs is not None:
-            evs[2].record(stream)
+    def window_args(w):
+        return dict(window=w) if w is not None else dict(down=args.down, up=args.up)
 
+    def step(evs=None):
+        k = 0
+        for key, X in acts.items():
+            if evs is not None:
+                evs[k].record(stream)
+            hs.hdiag(X, h=hbuf[key], workspace=ws, stream=stream)
+            k += 1
+        if evs is not None:
+            evs[k].record(stream)
+        k += 1
+        for (lname, W, xk, s_g, w), (codes, packed) in zip(layers, outs):
+            hs.search(W, hbuf[xk], s_g, init=args.init, scale_codes=codes, packed_e2m1=packed, stream=stream,
+                      **window_args(w))
+            if evs is not None:
+                evs[k].record(stream)
+            k += 1
+
+    n_ev = len(acts) + 1 + len(layers)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -150,9 +195,10 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    t_h = np.array([e[0].elapsed_time(e[1]) for e in events]) * 1e-3
-    t_s = np.array([e[1].elapsed_time(e[2]) for e in events]) * 1e-3
-    t_step = np.array([e[0].elapsed_time(e[2]) for e in events]) * 1e-3
+    nh = len(acts)
+    t_h = np.array([e[0].elapsed_time(e[nh]) for e in events]) * 1e-3  # all hdiag calls of a step
+    t_s = np.array([e[nh].elapsed_time(e[-1]) for e in events]) * 1e-3  # all search calls of a step
+    t_step = np.array([e[0].elapsed_time(e[-1]) for e in events]) * 1e-3
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         src.fill_(1)
@@ -166,30 +212,36 @@ def main():
                           "search_ms": float(t_s.mean() * 1e3)}), flush=True)
         return
 
-    weights = m * n
-    hd_bytes = 2.0 * T * n + 4.0 * n
+    weights = sum(W.numel() for (_, W, _, _, _) in layers)
+    hd_bytes = float(sum(2.0 * X.numel() + 4.0 * X.shape[1] for X in acts.values()))
     hd_gbs = hd_bytes / t_h.mean() / 1e9
     search_gws = weights / t_s.mean() / 1e9
-    ops = search_ops_per_weight(K) * weights
+    ops = 0
+    windows = []
+    for (_, W, _, _, w) in layers:
+        K = 2 * w + 1 if w is not None else args.down + args.up + 1
+        windows.append(w if w is not None else [args.down, args.up])
+        ops += search_ops_per_weight(K, args.init) * W.numel()
     search_tops = ops / t_s.mean() / 1e12
     search_gbs = SEARCH_BYTES_PER_WEIGHT * weights / t_s.mean() / 1e9
 
     rl_hdiag = {"bound": "hbm", "achieved": round(hd_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(hd_gbs / HBM_PEAK_GBS, 4), "traffic": None,
                 "kernel": "hscale_hdiag (hdiag_partial + hdiag_tree)",
-                "algorithmic_bytes_per_launch": hd_bytes, "avg_launch_ms": round(t_h.mean() * 1e3, 4)}
+                "algorithmic_bytes_per_step": hd_bytes, "avg_ms_per_step": round(t_h.mean() * 1e3, 4),
+                "launches_per_step": nh}
     rl_search = {"bound": "alu", "achieved": round(search_tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
                  "unit": "T lane-ops/s", "frac": round(search_tops / VALU_PEAK_TOPS, 4), "traffic": None,
                  "kernel": "hscale_search (search_kernel)",
-                 "algorithmic_ops_per_launch": ops, "ops_per_weight": search_ops_per_weight(K),
-                 "hbm_GBps": round(search_gbs, 1), "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4),
-                 "avg_launch_ms": round(t_s.mean() * 1e3, 4)}
-    traffic = measured_traffic(wl.name if window == 4 else "")
+                 "algorithmic_ops_per_step": ops, "hbm_GBps": round(search_gbs, 1),
+                 "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
+                 "launches_per_step": len(layers)}
+    default_shape = args.init == "maxabs" and args.down is None and args.window is None
+    traffic = measured_traffic(args.workload) if default_shape else None
     if traffic:
         rl_hdiag["traffic"] = traffic["hdiag"]
         rl_search["traffic"] = traffic["search"]
-        rl_hdiag["traffic_source"] = rl_search["traffic_source"] = os.path.relpath(
-            PROFILE_JSON, os.path.dirname(os.path.abspath(__file__)))
+        rl_hdiag["traffic_source"] = rl_search["traffic_source"] = traffic["source"]
     dominant = rl_hdiag if t_h.mean() >= t_s.mean() else rl_search
 
     out = {
@@ -205,8 +257,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: W {m}x{n} bf16 ({wl.w_dist}), X {T}x{n} bf16, window +-{window}",
-                   "out": m, "in": n, "tokens": T, "window": window, "global_scale": s_g},
+        "config": {"workload": desc, "name": args.workload, "layers": [l for (l, _, _, _, _) in layers],
+                   "weights": weights, "tokens": [X.shape[0] for X in acts.values()],
+                   "windows": windows, "init": args.init},
         "hdiag": {"GBps": round(hd_gbs, 1), "frac_of_peak": round(hd_gbs / HBM_PEAK_GBS, 4),
                   "ms": round(t_h.mean() * 1e3, 4)},
         "search": {"Gweights_per_s": round(search_gws, 2), "ms": round(t_s.mean() * 1e3, 4),
@@ -216,52 +269,55 @@ def main():
         "roofline": dominant,
         "rooflines": {"hdiag": rl_hdiag, "search": rl_search},
     }
-
     if not args.no_cpu_baseline:
-        out.update(cpu_leg(args, wl, X, W, h, codes, packed, s_g, window, tensor_bits))
-
+        out.update(cpu_leg(args, acts, layers, outs, hbuf))
     print(json.dumps(out), flush=True)
 
 
-def cpu_leg(args, wl, X, W, h, codes, packed, s_g, window, tensor_bits):
+def cpu_leg(args, acts, layers, outs, hbuf):
     """The oracle on a bounded sample of the same workload, on this host's
-    cores; the same rows double as a parity check of the benchmarked run."""
-    import torch
+    cores: rows of the last layer's W and tokens of its X.  The same rows are
+    checked for parity against the benchmarked outputs."""
+    import paper_2608_28113_amd as hs
     import oracle
+    from synth.workloads import tensor_bits
     from tests import parity
 
-    rows = min(args.cpu_rows, wl.out)
-    tok = min(args.cpu_tokens, wl.tokens)
+    lname, W, xk, s_g, w = layers[-1]
+    codes, packed = outs[-1]
+    X = acts[xk]
+    rows = min(args.cpu_rows, W.shape[0])
+    tok = min(args.cpu_tokens, X.shape[0])
+    down, up = (w, w) if w is not None else (args.down, args.up)
+    init = "4over6" if args.init == "4over6" else "rtn"
     Wb = tensor_bits(W[:rows])
-    h32 = h.cpu().numpy()
+    h32 = hbuf[xk].cpu().numpy()
     Xb = tensor_bits(X[:tok])
     oracle._load()
     t0 = time.perf_counter()
-    r = oracle.search(Wb, h32, s_g, window=window)
+    oracle.search(Wb, h32, s_g, down=down, up=up, init=init)
     t_search = time.perf_counter() - t0
     t0 = time.perf_counter()
     href = oracle.hdiag(Xb)
     t_hd = time.perf_counter() - t0
-    rep = parity.compare_search(Wb, h32, s_g, window, window, codes[:rows].cpu().numpy(),
-                                packed[:rows].cpu().numpy())
-    # h on the full X cannot be recomputed here cheaply; check the sample's
-    # columns against a GPU hdiag of the same token slice.
-    import paper_2608_28113_amd as hs
+    rep = parity.compare_search(Wb, h32, s_g, down, up, codes[:rows].cpu().numpy(), packed[:rows].cpu().numpy(),
+                                init=init)
     h_slice = hs.hdiag(X[:tok].contiguous()).cpu().numpy()
     hrep = parity.compare_h(h_slice, href)
     return {
         "cpu_baseline": {
             "value": round(Wb.size / t_search / 1e9, 6), "unit": "Gweights/s", "cores": 1, "kind": "oracle",
-            "sample": f"search on rows 0..{rows - 1} of W ({Wb.size} weights, window +-{window}, "
-                      f"{t_search:.2f} s); hdiag on tokens 0..{tok - 1} of X ({Xb.nbytes / 1e9:.2f} GB, "
-                      f"{t_hd:.2f} s, {Xb.nbytes / t_hd / 1e9:.2f} GB/s)",
+            "sample": f"search on rows 0..{rows - 1} of {lname} ({Wb.size} weights, shifts -{down}..+{up}, "
+                      f"init {init}, {t_search:.2f} s); hdiag on tokens 0..{tok - 1} of its X "
+                      f"({Xb.nbytes / 1e9:.2f} GB, {t_hd:.2f} s, {Xb.nbytes / t_hd / 1e9:.2f} GB/s)",
             "hdiag_GBps": round(Xb.nbytes / t_hd / 1e9, 3),
             "cpu_model": _cpu_model(),
             "host_cpus": os.cpu_count(),
         },
-        "parity": {"search_rows_checked": rows, "groups": rep["groups"], "near_ties": rep["near_ties"],
-                   "mismatches": rep["mismatches"], "ok": rep["ok"],
-                   "hdiag_tokens_checked": tok, "hdiag_max_rel": hrep["max_rel"], "hdiag_ok": hrep["ok"]},
+        "parity": {"layer": lname, "search_rows_checked": rows, "groups": rep["groups"],
+                   "near_ties": rep["near_ties"], "init_ties": rep["init_ties"], "mismatches": rep["mismatches"],
+                   "ok": rep["ok"], "hdiag_tokens_checked": tok, "hdiag_max_rel": hrep["max_rel"],
+                   "hdiag_ok": hrep["ok"]},
     }
 
 
