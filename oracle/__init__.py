@@ -75,6 +75,9 @@ def _load():
     lib.oracle_search_init.argtypes = [P, i64, i64, P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                        ctypes.c_int, P, P, P, P, P, P, P, P]
     lib.oracle_search_init.restype = ctypes.c_int
+    lib.oracle_search_stats.argtypes = [P, i64, i64, P, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                        ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_search_stats.restype = ctypes.c_int
     lib.oracle_anchor_codes.argtypes = [P, i64, i64, ctypes.c_float, ctypes.c_double, P]
     lib.oracle_anchor_codes.restype = ctypes.c_int
     lib.oracle_hdiag_accumulate.argtypes = [P, i64, i64, P]
@@ -88,6 +91,12 @@ def _load():
     lib.oracle_group_search.argtypes = [P, P, ctypes.c_int, ctypes.c_float,
                                         ctypes.c_int, ctypes.c_int, P, P, P, P]
     lib.oracle_group_search.restype = ctypes.c_int
+    lib.oracle_delta.argtypes = [P, i64, i64, ctypes.c_float, P, P, P]
+    lib.oracle_delta.restype = ctypes.c_int
+    lib.oracle_output_error.argtypes = [P, i64, i64, P, i64, P]
+    lib.oracle_output_error.restype = ctypes.c_int
+    lib.oracle_shift_summary.argtypes = [P, P, P, i64, ctypes.c_int, ctypes.c_int, P, P, P, P]
+    lib.oracle_shift_summary.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -165,8 +174,10 @@ def search(W, h, s_g: float, window: int | None = None, down: int | None = None,
     ``init`` is "rtn" (max-abs, Eq. 7), "4over6" (the better of max/4 and
     max/6 under plain MSE), or a uint8 array [m, n/16] of initial codes.
     Returns codes [m, n/16] u8, packed [m, n/2] u8, e_best / e_second
-    [m, n/16] f64, c0 [m, n/16] u8 (the initial codes) and, for "4over6",
-    l4 / l6 [m, n/16] f64 (the two anchors' plain squared errors).
+    [m, n/16] f64, c0 [m, n/16] u8 (the initial codes), shift [m, n/16] i8
+    (the chosen shift d*), e_init [m, n/16] f64 (the error at d = 0) and,
+    for "4over6", l4 / l6 [m, n/16] f64 (the two anchors' plain squared
+    errors).
     """
     if window is not None:
         down = up = int(window)
@@ -189,13 +200,16 @@ def search(W, h, s_g: float, window: int | None = None, down: int | None = None,
     c0 = np.zeros((m, G), np.uint8)
     l4 = np.zeros((m, G), np.float64)
     l6 = np.zeros((m, G), np.float64)
-    rc = _load().oracle_search_init(_ptr(W), m, n, _ptr(h), int(down), int(up),
-                                    np.float32(s_g), mode, _ptr(init_codes), _ptr(codes),
-                                    _ptr(packed), _ptr(e_best), _ptr(e_second), _ptr(c0),
-                                    _ptr(l4), _ptr(l6))
+    shift = np.zeros((m, G), np.int8)
+    e_init = np.zeros((m, G), np.float64)
+    rc = _load().oracle_search_stats(_ptr(W), m, n, _ptr(h), int(down), int(up),
+                                     np.float32(s_g), mode, _ptr(init_codes), _ptr(codes),
+                                     _ptr(packed), _ptr(e_best), _ptr(e_second), _ptr(c0),
+                                     _ptr(l4), _ptr(l6), _ptr(shift), _ptr(e_init))
     if rc != 0:
-        raise ValueError("oracle_search_init: bad arguments")
-    out = dict(codes=codes, packed=packed, e_best=e_best, e_second=e_second, c0=c0)
+        raise ValueError("oracle_search_stats: bad arguments")
+    out = dict(codes=codes, packed=packed, e_best=e_best, e_second=e_second, c0=c0,
+               shift=shift, e_init=e_init)
     if mode == INIT_4OVER6:
         out.update(l4=l4, l6=l6)
     return out
@@ -299,3 +313,47 @@ def unpack_nibbles(packed: np.ndarray) -> np.ndarray:
     out[..., 0::2] = packed & 0xF
     out[..., 1::2] = packed >> 4
     return out
+
+
+def delta(W, s_g: float, codes, packed) -> np.ndarray:
+    """Rounding error W - W^ of a stored NVFP4 tensor, fp64 [m, n]."""
+    W = _bf16_bits(W)
+    m, n = W.shape
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    assert codes.shape == (m, n // 16) and packed.shape == (m, n // 2)
+    out = np.zeros((m, n), np.float64)
+    if _load().oracle_delta(_ptr(W), m, n, np.float32(s_g), _ptr(codes), _ptr(packed), _ptr(out)) != 0:
+        raise ValueError("oracle_delta: bad arguments")
+    return out
+
+
+def output_error(X, dW, row_err: np.ndarray | None = None) -> np.ndarray:
+    """Eq. 3 per output row: row_err[r] += sum_t (X dW^T)_tr^2 (fp64 [m])."""
+    X = _bf16_bits(X)
+    T, n = X.shape
+    dW = np.ascontiguousarray(dW, dtype=np.float64)
+    m = dW.shape[0]
+    assert dW.shape == (m, n)
+    if row_err is None:
+        row_err = np.zeros(m, np.float64)
+    assert row_err.dtype == np.float64 and row_err.shape == (m,) and row_err.flags["C_CONTIGUOUS"]
+    if _load().oracle_output_error(_ptr(X), T, n, _ptr(dW), m, _ptr(row_err)) != 0:
+        raise ValueError("oracle_output_error: bad arguments")
+    return row_err
+
+
+def shift_summary(shift, e_best, e_init, down: int, up: int) -> dict:
+    """Per-shift counts, sums of initial / chosen errors and of relative
+    reductions (bins d = -down..up)."""
+    shift = np.ascontiguousarray(shift, dtype=np.int8).ravel()
+    e_best = np.ascontiguousarray(e_best, dtype=np.float64).ravel()
+    e_init = np.ascontiguousarray(e_init, dtype=np.float64).ravel()
+    K = down + up + 1
+    count = np.zeros(K, np.int64)
+    si, sb, sr = (np.zeros(K, np.float64) for _ in range(3))
+    rc = _load().oracle_shift_summary(_ptr(shift), _ptr(e_best), _ptr(e_init), shift.size, int(down), int(up),
+                                      _ptr(count), _ptr(si), _ptr(sb), _ptr(sr))
+    if rc != 0:
+        raise ValueError("oracle_shift_summary: bad arguments")
+    return dict(count=count, sum_init=si, sum_best=sb, sum_rel=sr)

@@ -21,6 +21,7 @@
  * Paper sections followed (H-Scale, Hessian-guided scale refinement for
  * NVFP4):
  *   Sec. 3.1, Eq. 1-2   effective scale s = s_g * l and the FP4 quantizer
+ *   Sec. 3.2, Eq. 3     layer-output error ||X dW^T||^2 (quality diagnostics)
  *   Sec. 3.2, Eq. 4     h = diag(X^T X)
  *   Sec. 3.2, Eq. 6     per-group weighted objective ||(w - w^) . sqrt(h)||^2
  *   Sec. 3.3, Eq. 7     l_init = Q_fp8(s_init / s_g), s_init from the group max
@@ -28,6 +29,8 @@
  *   Sec. 3.3, Eq. 12-13 FP4 quantization per candidate and the argmin
  *   Sec. 3.3 "Final re-quantization"
  *   App. B, Alg. HScaleGroupQuantize (the same steps as pseudocode)
+ *   App. "Selected Scale Shifts" and "Candidate-Window Width" (statistics
+ *                       of the chosen shift; L_full of a window)
  *
  * Readings where the paper is silent (each stated where it is used):
  *   E4M3 is OCP E4M3FN (max 448, 126 positive finite codes); Q_fp8 rounds to
@@ -43,6 +46,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define ORACLE_M 126 /* positive finite E4M3FN codes 1..126 */
@@ -166,6 +170,12 @@ double oracle_quantize_group(const double *w, const int *neg, const double *h,
     return err;
 }
 
+int oracle_walk_group_d(const double *w, const int *neg, const double *h,
+                        int g, int c0, int down, int up, const float *S,
+                        const float *R, uint8_t *nib_out, double *e_best,
+                        double *e_second, int *cand_codes, double *cand_err,
+                        int *shift_out, double *e_init);
+
 /* The walk of Eq. 9-13 from a given initial ladder index c0 (Alg.
  * HScaleGroupQuantize takes the baseline's initial scale as an input).
  * Candidate codes are clip(c0 + d, 1, M) for d = -down..up in increasing d;
@@ -177,7 +187,20 @@ int oracle_walk_group(const double *w, const int *neg, const double *h, int g,
                       int c0, int down, int up, const float *S,
                       const float *R, uint8_t *nib_out, double *e_best,
                       double *e_second, int *cand_codes, double *cand_err) {
-    int best_c = 0;
+    return oracle_walk_group_d(w, neg, h, g, c0, down, up, S, R, nib_out,
+                               e_best, e_second, cand_codes, cand_err, NULL,
+                               NULL);
+}
+
+/* The walk, also reporting the chosen shift d* (the first minimum, as in
+ * the paper's selected-shift statistics) and the error at d = 0, the
+ * initial code's error. */
+int oracle_walk_group_d(const double *w, const int *neg, const double *h,
+                        int g, int c0, int down, int up, const float *S,
+                        const float *R, uint8_t *nib_out, double *e_best,
+                        double *e_second, int *cand_codes, double *cand_err,
+                        int *shift_out, double *e_init) {
+    int best_c = 0, best_d = -down;
     double best_e = 0.0;
     int k = 0;
     for (int d = -down; d <= up; ++d, ++k) {
@@ -187,11 +210,14 @@ int oracle_walk_group(const double *w, const int *neg, const double *h, int g,
         double e = oracle_quantize_group(w, neg, h, g, S[c], R[c], NULL);
         if (cand_codes) cand_codes[k] = c;
         if (cand_err) cand_err[k] = e;
+        if (d == 0 && e_init) *e_init = e;
         if (d == -down || e < best_e) {
             best_e = e;
             best_c = c;
+            best_d = d;
         }
     }
+    if (shift_out) *shift_out = best_d;
     double second = INFINITY;
     for (int d = -down; d <= up; ++d) {
         int c = c0 + d;
@@ -297,6 +323,13 @@ static void store_nibbles(uint8_t *packed, int64_t n, int64_t r, int64_t i,
         dst[k] = (uint8_t)(nib[2 * k] | (nib[2 * k + 1] << 4));
 }
 
+int oracle_search_stats(const uint16_t *W, int64_t m, int64_t n, const float *h,
+                        int down, int up, float s_g, int init_mode,
+                        const uint8_t *init_codes, uint8_t *codes,
+                        uint8_t *packed, double *e_best, double *e_second,
+                        uint8_t *c0, double *l4, double *l6, int8_t *shift,
+                        double *e_init);
+
 /* Initial-code rules for the matrix-level search. */
 #define ORACLE_INIT_RTN 0      /* max-abs scale, Eq. 7 */
 #define ORACLE_INIT_4OVER6 1   /* the better of max/4 and max/6 (plain MSE) */
@@ -313,6 +346,19 @@ int oracle_search_init(const uint16_t *W, int64_t m, int64_t n, const float *h,
                        const uint8_t *init_codes, uint8_t *codes,
                        uint8_t *packed, double *e_best, double *e_second,
                        uint8_t *c0, double *l4, double *l6) {
+    return oracle_search_stats(W, m, n, h, down, up, s_g, init_mode, init_codes,
+                               codes, packed, e_best, e_second, c0, l4, l6,
+                               NULL, NULL);
+}
+
+/* oracle_search_init plus the chosen shift per group (int8 [m, n/16]) and
+ * the initial code's error (fp64 [m, n/16]), both optional. */
+int oracle_search_stats(const uint16_t *W, int64_t m, int64_t n, const float *h,
+                        int down, int up, float s_g, int init_mode,
+                        const uint8_t *init_codes, uint8_t *codes,
+                        uint8_t *packed, double *e_best, double *e_second,
+                        uint8_t *c0, double *l4, double *l6, int8_t *shift,
+                        double *e_init) {
     if (n % 16 != 0 || down < 0 || up < 0 || !(s_g > 0.0f)) return -1;
     if (init_mode < 0 || init_mode > 2) return -1;
     if (init_mode == ORACLE_INIT_GIVEN && !init_codes) return -1;
@@ -338,9 +384,12 @@ int oracle_search_init(const uint16_t *W, int64_t m, int64_t n, const float *h,
                 if (c0v < 1) c0v = 1;
                 if (c0v > ORACLE_M) c0v = ORACLE_M;
             }
-            double eb, es;
-            int c = oracle_walk_group(w, neg, hh, 16, c0v, down, up, S, R, nib,
-                                      &eb, &es, NULL, NULL);
+            double eb, es, ei = 0.0;
+            int dstar = 0;
+            int c = oracle_walk_group_d(w, neg, hh, 16, c0v, down, up, S, R, nib,
+                                        &eb, &es, NULL, NULL, &dstar, &ei);
+            if (shift) shift[r * G + i] = (int8_t)dstar;
+            if (e_init) e_init[r * G + i] = ei;
             codes[r * G + i] = (uint8_t)c;
             store_nibbles(packed, n, r, i, nib);
             if (e_best) e_best[r * G + i] = eb;
@@ -473,4 +522,93 @@ int oracle_group_search(const double *w, const double *h, int g, float s_g,
     if (nib)
         for (int j = 0; j < g; ++j) nib[j] = tmp[j];
     return c;
+}
+
+/* ------------------------------------------------------------------------
+ * Quality diagnostics (Sec. 3.2 Eq. 3; App. "Selected Scale Shifts" and
+ * "Candidate-Window Width")
+ * ---------------------------------------------------------------------- */
+
+/* The rounding error Delta W = W - W^ of a stored NVFP4 tensor, in fp64:
+ * element (r, j) of group i = j / 16 is w - v * S[c] with c the group's
+ * scale code, v the signed E2M1 value of its nibble and S[c] the fp32
+ * effective scale of Eq. 1 (S[0] = 0).  The fp64 value is exact: v has two
+ * significant bits and S 24, and |w| / S stays below 2^21 for codes >= 1.
+ * codes [m, n/16] in 0..M, packed [m, n/2] (element 2k in the low nibble),
+ * delta [m, n] row-major. */
+int oracle_delta(const uint16_t *W, int64_t m, int64_t n, float s_g,
+                 const uint8_t *codes, const uint8_t *packed, double *delta) {
+    if (n % 16 != 0 || !(s_g > 0.0f)) return -1;
+    float S[ORACLE_M + 1], R[ORACLE_M + 1];
+    oracle_scale_tables(s_g, S, R);
+    int64_t G = n / 16;
+    for (int64_t r = 0; r < m; ++r) {
+        for (int64_t j = 0; j < n; ++j) {
+            int c = codes[r * G + j / 16];
+            if (c > ORACLE_M) return -1;
+            uint8_t byte = packed[r * (n / 2) + j / 2];
+            int nib = (j % 2 == 0) ? (byte & 15) : (byte >> 4);
+            double v = kE2M1[nib & 7];
+            if (nib & 8) v = -v;
+            uint32_t bits = (uint32_t)W[r * n + j] << 16;
+            float wf;
+            memcpy(&wf, &bits, sizeof wf);
+            delta[r * n + j] = (double)wf - v * (double)S[c];
+        }
+    }
+    return 0;
+}
+
+/* Eq. 3, the layer-output error of Delta W on calibration activations X,
+ * split by output row: row_err[r] += sum_t (sum_j x_tj * Delta_rj)^2.  The
+ * total over r is ||X Delta W^T||_F^2 = Tr(Delta W X^T X Delta W^T), the
+ * L_full the paper uses to score a window.  X bf16 [T, n] row-major; delta
+ * fp64 [m, n]; plain fp64 loops in t, then j. */
+int oracle_output_error(const uint16_t *X, int64_t T, int64_t n,
+                        const double *delta, int64_t m, double *row_err) {
+    if (T < 0 || n < 0 || m < 0) return -1;
+    double *x = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    if (!x) return -1;
+    for (int64_t t = 0; t < T; ++t) {
+        for (int64_t j = 0; j < n; ++j) {
+            uint32_t bits = (uint32_t)X[t * n + j] << 16;
+            float xf;
+            memcpy(&xf, &bits, sizeof xf);
+            x[j] = (double)xf;
+        }
+        for (int64_t r = 0; r < m; ++r) {
+            double y = 0.0;
+            for (int64_t j = 0; j < n; ++j) y += x[j] * delta[r * n + j];
+            row_err[r] += y * y;
+        }
+    }
+    free(x);
+    return 0;
+}
+
+/* The selected-shift statistics: for every shift d = -down..up (bin
+ * d + down), the number of groups that chose it, the sums of their errors
+ * at d = 0 and at the chosen shift, and the sum of their relative
+ * reductions (e_init - e_best) / e_init (0 for a group whose initial error
+ * is 0).  The mean reduction of a bin is sum_rel / count; the fraction of
+ * the initial error removed is 1 - sum(sum_best) / sum(sum_init). */
+int oracle_shift_summary(const int8_t *shift, const double *e_best,
+                         const double *e_init, int64_t groups, int down,
+                         int up, int64_t *count, double *sum_init,
+                         double *sum_best, double *sum_rel) {
+    if (groups < 0 || down < 0 || up < 0) return -1;
+    for (int k = 0; k <= down + up; ++k) {
+        count[k] = 0;
+        sum_init[k] = sum_best[k] = sum_rel[k] = 0.0;
+    }
+    for (int64_t g = 0; g < groups; ++g) {
+        int d = shift[g];
+        if (d < -down || d > up) return -1;
+        int k = d + down;
+        count[k] += 1;
+        sum_init[k] += e_init[g];
+        sum_best[k] += e_best[g];
+        if (e_init[g] > 0.0) sum_rel[k] += (e_init[g] - e_best[g]) / e_init[g];
+    }
+    return 0;
 }

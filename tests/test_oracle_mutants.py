@@ -49,6 +49,19 @@ MUTANTS = {
                               "            h[j] = x * x;\n        }\n    }\n}\n\n/* Loads group"),
     "zero_drops_sign": ("if (nib) nib[j] = (uint8_t)((neg[j] << 3) | i);",
                         "if (nib) nib[j] = (uint8_t)(((neg[j] && i) << 3) | i);"),
+    "delta_sign": ("delta[r * n + j] = (double)wf - v * (double)S[c];",
+                   "delta[r * n + j] = (double)wf + v * (double)S[c];"),
+    "delta_nibble_order": ("int nib = (j % 2 == 0) ? (byte & 15) : (byte >> 4);",
+                           "int nib = (j % 2 == 0) ? (byte >> 4) : (byte & 15);"),
+    "output_error_not_squared": ("row_err[r] += y * y;", "row_err[r] += fabs(y);"),
+    "output_error_reversed_column": ("y += x[j] * delta[r * n + j];", "y += x[j] * delta[r * n + (n - 1 - j)];"),
+    "output_error_overwrites": ("row_err[r] += y * y;", "row_err[r] = y * y;"),
+    "summary_rel_wrong_denominator": ("sum_rel[k] += (e_init[g] - e_best[g]) / e_init[g];",
+                                      "sum_rel[k] += (e_init[g] - e_best[g]) / e_best[g];"),
+    "summary_swaps_sums": ("sum_init[k] += e_init[g];\n        sum_best[k] += e_best[g];",
+                           "sum_init[k] += e_best[g];\n        sum_best[k] += e_init[g];"),
+    "stats_shift_not_first_min": ("            best_c = c;\n            best_d = d;",
+                                  "            best_c = c;\n            best_d = d - (d > 0);"),
 }
 
 
@@ -65,6 +78,7 @@ def test_pins_catch_planted_mistake(name, tmp_path):
     env = dict(os.environ, HSCALE_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", str(ROOT / "tests" / "test_oracle_pins.py"),
                         str(ROOT / "tests" / "test_oracle_pins_init.py"),
+                        str(ROOT / "tests" / "test_oracle_pins_diag.py"),
                         "-q", "-x", "-p", "no:cacheprovider"],
                        capture_output=True, text=True, env=env, cwd=str(ROOT), timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"

@@ -135,3 +135,20 @@ def test_anchor_codes():
     assert np.array_equal(oracle.anchor_codes(Wb, s_g, 6.0), libref.rtn_codes(Wb, s_g, 6.0))
     assert np.array_equal(oracle.anchor_codes(Wb, s_g, 4.0), libref.rtn_codes(Wb, s_g, 4.0))
     assert np.array_equal(oracle.anchor_codes(Wb, s_g, 6.0), oracle.search(Wb, h, s_g, window=0)["c0"])
+
+
+def test_shift_and_initial_error():
+    """The chosen shift d* and the error at d = 0 (the selected-shift and
+    error-removed statistics of Sec. 4's ablation figure)."""
+    Wb, h, s_g = _tiny_inputs()
+    for init in ("rtn", "4over6"):
+        r = oracle.search(Wb, h, s_g, down=9, up=6, init=init)
+        d = r["shift"].astype(np.int64)
+        assert d.min() >= -9 and d.max() <= 6
+        assert np.array_equal(np.clip(r["c0"].astype(np.int64) + d, 1, 126), r["codes"])
+        _, e0 = oracle.quantize(Wb, s_g, r["c0"], h)
+        assert np.allclose(r["e_init"], e0, rtol=1e-12)
+        assert np.all(r["e_best"] <= r["e_init"])
+        assert np.array_equal(r["e_best"] == r["e_init"], d == 0) or np.all(r["e_best"][d != 0] < r["e_init"][d != 0])
+        r0 = oracle.search(Wb, h, s_g, window=0, init=init)
+        assert np.all(r0["shift"] == 0) and np.array_equal(r0["e_init"], r0["e_best"])
