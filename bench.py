@@ -270,37 +270,44 @@ def main():
         "rooflines": {"hdiag": rl_hdiag, "search": rl_search},
     }
     if not args.no_cpu_baseline:
-        out.update(cpu_leg(args, acts, layers, outs, hbuf))
+        out.update(cpu_leg(args, acts, layers))
     print(json.dumps(out), flush=True)
 
 
-def cpu_leg(args, acts, layers, outs, hbuf):
+def cpu_leg(args, acts, layers):
     """The oracle on a bounded sample of the same workload, on this host's
-    cores: rows of the last layer's W and tokens of its X.  The same rows are
-    checked for parity against the benchmarked outputs."""
+    cores: rows of the last layer's W and tokens of its X.
+
+    Parity: h for the check is the oracle's, over the sampled tokens, rounded
+    to fp32 (no oracle input comes from the HIP path).  The HIP search runs
+    again, untimed, on the whole last layer in the launch configuration the
+    timed steps use, with that h; its sampled rows must match the oracle's
+    search.  The HIP hdiag of the sampled tokens is checked against the
+    oracle's h."""
+    import torch
     import paper_2608_28113_amd as hs
     import oracle
     from synth.workloads import tensor_bits
     from tests import parity
 
     lname, W, xk, s_g, w = layers[-1]
-    codes, packed = outs[-1]
     X = acts[xk]
     rows = min(args.cpu_rows, W.shape[0])
     tok = min(args.cpu_tokens, X.shape[0])
     down, up = (w, w) if w is not None else (args.down, args.up)
     init = "4over6" if args.init == "4over6" else "rtn"
     Wb = tensor_bits(W[:rows])
-    h32 = hbuf[xk].cpu().numpy()
     Xb = tensor_bits(X[:tok])
     oracle._load()
     t0 = time.perf_counter()
-    oracle.search(Wb, h32, s_g, down=down, up=up, init=init)
-    t_search = time.perf_counter() - t0
-    t0 = time.perf_counter()
     href = oracle.hdiag(Xb)
     t_hd = time.perf_counter() - t0
-    rep = parity.compare_search(Wb, h32, s_g, down, up, codes[:rows].cpu().numpy(), packed[:rows].cpu().numpy(),
+    h_in = href.astype(np.float32)
+    t0 = time.perf_counter()
+    oracle.search(Wb, h_in, s_g, down=down, up=up, init=init)
+    t_search = time.perf_counter() - t0
+    codes, packed = hs.search(W, torch.from_numpy(h_in).to(W.device), s_g, down=down, up=up, init=args.init)
+    rep = parity.compare_search(Wb, h_in, s_g, down, up, codes[:rows].cpu().numpy(), packed[:rows].cpu().numpy(),
                                 init=init)
     h_slice = hs.hdiag(X[:tok].contiguous()).cpu().numpy()
     hrep = parity.compare_h(h_slice, href)
@@ -314,7 +321,8 @@ def cpu_leg(args, acts, layers, outs, hbuf):
             "cpu_model": _cpu_model(),
             "host_cpus": os.cpu_count(),
         },
-        "parity": {"layer": lname, "search_rows_checked": rows, "groups": rep["groups"],
+        "parity": {"layer": lname, "h_source": f"oracle hdiag of tokens 0..{tok - 1}, fp32",
+                   "search_rows_checked": rows, "groups": rep["groups"],
                    "near_ties": rep["near_ties"], "init_ties": rep["init_ties"], "mismatches": rep["mismatches"],
                    "ok": rep["ok"], "hdiag_tokens_checked": tok, "hdiag_max_rel": hrep["max_rel"],
                    "hdiag_ok": hrep["ok"]},

@@ -17,7 +17,9 @@
  * search from baseline-provided initial scales (HScaleGroupQuantize takes
  * them as input), the 4over6 initialisation, a strided column-block form for
  * GPTQ-style blockwise use, and h accumulated over streamed calibration
- * batches.
+ * batches.  Quality diagnostics of the appendix: the search with per-group
+ * statistics (chosen shift, its error, the error at shift 0) and their
+ * per-shift summary.
  *
  * Conventions shared by every entry point
  *   - All pointers are device pointers (hipMalloc'd or torch CUDA tensors)
@@ -211,6 +213,60 @@ int hscale_search_block(const void *W, int64_t ldw, int64_t out,
                         uint8_t *scale_codes, int64_t ldc,
                         uint8_t *packed_e2m1, int64_t ldp,
                         hipStream_t stream);
+
+/*
+ * The search with per-group statistics, for the selected-shift analysis of
+ * the paper's appendix (which shift each group chose and how much of the
+ * initial error it removed).  Writes scale_codes and packed_e2m1 exactly as
+ * hscale_search_block with contiguous strides and the same init_mode /
+ * init_codes ([out, in / 16] when HSCALE_INIT_GIVEN), and, for group
+ * g = r * (in / 16) + k:
+ *
+ * shift      int8 [out, in / 16]: the chosen shift d* in -down .. up (the
+ *            first minimum; code = clip(c0 + d*, 1, 126))
+ * err_best   fp32 [out, in / 16]: the score E at d*, as the search computed it
+ * err_init   fp32 [out, in / 16]: the score E at d = 0 (the initial code)
+ *
+ * All three are required (4-byte aligned errors) and must not overlap any
+ * other buffer.  The kernel is the search kernel with these three extra
+ * stores; the plain entry points do not pay for them.
+ */
+int hscale_search_stats(const void *W, int64_t out, int64_t in, const float *h,
+                        int32_t down, int32_t up, float global_scale,
+                        int32_t init_mode, const uint8_t *init_codes,
+                        uint8_t *scale_codes, uint8_t *packed_e2m1,
+                        int8_t *shift, float *err_best, float *err_init,
+                        hipStream_t stream);
+
+/* Workspace bytes hscale_shift_summary needs (0 when groups <= 0). */
+size_t hscale_shift_summary_workspace_bytes(int64_t groups, int32_t down,
+                                            int32_t up);
+
+/*
+ * Per-shift summary of hscale_search_stats' outputs (the appendix's
+ * selected-shift figure): for bin k = d + down, d = -down .. up,
+ *   count[k]     uint64: groups whose shift is d
+ *   sum_init[k]  fp64: sum of their err_init
+ *   sum_best[k]  fp64: sum of their err_best
+ *   sum_rel[k]   fp64: sum of (err_init - err_best) / err_init (0 when
+ *                err_init = 0); the bin's mean reduction is sum_rel / count
+ * The fraction of the initial error removed over all groups is
+ * 1 - sum(sum_best) / sum(sum_init).  Sums are formed in fp64 in a fixed
+ * order (bitwise reproducible).  Groups whose shift lies outside
+ * -down .. up are not counted.
+ *
+ * shift, err_best, err_init  [groups] as written by hscale_search_stats
+ *                            (needed only when groups > 0)
+ * count, sum_init, sum_best, sum_rel  [down + up + 1] each, 8-byte aligned,
+ *                            always written (all zero when groups = 0)
+ * workspace      >= hscale_shift_summary_workspace_bytes(groups, down, up)
+ *                bytes, 8-byte aligned, scratch owned by the caller
+ */
+int hscale_shift_summary(const int8_t *shift, const float *err_best,
+                         const float *err_init, int64_t groups, int32_t down,
+                         int32_t up, uint64_t *count, double *sum_init,
+                         double *sum_best, double *sum_rel, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Final re-quantization at given scale codes (Sec. 3.3; Eq. 12 at a fixed

@@ -29,6 +29,9 @@ EXPORTS = (
     "hscale_search_4over6",
     "hscale_search_from",
     "hscale_search_block",
+    "hscale_search_stats",
+    "hscale_shift_summary_workspace_bytes",
+    "hscale_shift_summary",
     "hscale_quantize",
 )
 
@@ -75,6 +78,12 @@ def load() -> ctypes.CDLL:
     lib.hscale_search_from.restype = ctypes.c_int
     lib.hscale_search_block.argtypes = [P, i64, i64, i64, P, i32, i32, f32, i32, P, i64, P, i64, P, i64, P]
     lib.hscale_search_block.restype = ctypes.c_int
+    lib.hscale_search_stats.argtypes = [P, i64, i64, P, i32, i32, f32, i32, P, P, P, P, P, P, P]
+    lib.hscale_search_stats.restype = ctypes.c_int
+    lib.hscale_shift_summary_workspace_bytes.argtypes = [i64, i32, i32]
+    lib.hscale_shift_summary_workspace_bytes.restype = sz
+    lib.hscale_shift_summary.argtypes = [P, P, P, i64, i32, i32, P, P, P, P, P, sz, P]
+    lib.hscale_shift_summary.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -140,3 +149,23 @@ def hscale_search_block(W: int, ldw: int, out: int, cols: int, h: int, down: int
     return load().hscale_search_block(W or None, ldw, out, cols, h or None, down, up, global_scale,
                                       init_mode, init_codes or None, ldi, scale_codes or None, ldc,
                                       packed_e2m1 or None, ldp, stream or None)
+
+
+def hscale_search_stats(W: int, out: int, in_: int, h: int, down: int, up: int, global_scale: float,
+                        init_mode: int, init_codes: int, scale_codes: int, packed_e2m1: int, shift: int,
+                        err_best: int, err_init: int, stream: int) -> int:
+    return load().hscale_search_stats(W or None, out, in_, h or None, down, up, global_scale, init_mode,
+                                      init_codes or None, scale_codes or None, packed_e2m1 or None,
+                                      shift or None, err_best or None, err_init or None, stream or None)
+
+
+def hscale_shift_summary_workspace_bytes(groups: int, down: int, up: int) -> int:
+    return load().hscale_shift_summary_workspace_bytes(groups, down, up)
+
+
+def hscale_shift_summary(shift: int, err_best: int, err_init: int, groups: int, down: int, up: int,
+                         count: int, sum_init: int, sum_best: int, sum_rel: int, workspace: int,
+                         workspace_bytes: int, stream: int) -> int:
+    return load().hscale_shift_summary(shift or None, err_best or None, err_init or None, groups, down, up,
+                                       count or None, sum_init or None, sum_best or None, sum_rel or None,
+                                       workspace or None, workspace_bytes, stream or None)

@@ -353,11 +353,13 @@ __device__ __forceinline__ int anchor_code(float amax, float anchor, float s_g) 
 
 // Eq. 7 and 9-13 for one group held in registers: the initial code (by the
 // rule kInit; `given` is the caller's code for kInitGiven), then the walk
-// d = -down..up in pairs, keeping the first minimum.
-template <int kInit>
+// d = -down..up in pairs, keeping the first minimum.  With kStats it also
+// reports the chosen shift, its error and the error at d = 0.
+template <int kInit, bool kStats>
 __device__ __forceinline__ void search_group(const float (&w)[kGroup], const float (&hh)[kGroup],
                                              const ScaleEntry *tab, int down, int up, float s_g, int given,
-                                             int &code, uint2 &best_p) {
+                                             int &code, uint2 &best_p, int &shift, float &err_best,
+                                             float &err_init) {
     int c0;
     if (kInit == kInitGiven) {
         c0 = min(max(given, 1), kMaxCode);
@@ -378,7 +380,7 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
         }
     }
     const ScaleEntry *col = tab + (c0 + kTabPad);  // col[d] is candidate c0 + d, clipped
-    float best_e = 0.0f;
+    float best_e = 0.0f, e_init = 0.0f;
     int best_d = -down;
     best_p = make_uint2(0u, 0u);
     // Scratch words the conversions rewrite in place (all 8 bytes each time),
@@ -392,6 +394,10 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
         pb = quantize_group(w, sb.R, pb);
         const float ea = group_error(w, hh, pa, sa.S);
         const float eb = group_error(w, hh, pb, sb.S);
+        if (kStats) {
+            if (d == 0) e_init = ea;
+            if (d + 1 == 0) e_init = eb;
+        }
         if (d == -down || ea < best_e) {
             best_e = ea;
             best_d = d;
@@ -407,6 +413,7 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
         const ScaleEntry se = col[d];
         pa = quantize_group(w, se.R, pa);
         const float e = group_error(w, hh, pa, se.S);
+        if (kStats && d == 0) e_init = e;
         if (d == -down || e < best_e) {
             best_e = e;
             best_d = d;
@@ -414,6 +421,9 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
         }
     }
     code = min(max(c0 + best_d, 1), kMaxCode);
+    shift = best_d;
+    err_best = best_e;
+    err_init = e_init;
 }
 
 // Arguments of a search over a block of `rows` x (16 Gc) weights inside
@@ -435,13 +445,16 @@ struct SearchArgs {
     uint64_t ldc;
     uint2 *packed;
     uint64_t ldp_vec;
+    int8_t *shift;    // statistics, [rows * Gc] at index g (kStats only)
+    float *err_best;
+    float *err_init;
 };
 
 // One group per lane over the flat index g = r * Gc + i of the block, so the
 // lanes of a wave cover consecutive groups of a row (contiguous loads and
 // stores) and a lane's h slice is h[16 i .. 16 i + 15].  A launch normally
 // covers every group once; larger problems loop with a grid stride.
-template <int kInit>
+template <int kInit, bool kStats>
 __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs a) {
     __shared__ ScaleEntry tab[kTabSize];
     __shared__ ScaleEntry uniq[kMaxCode + 1];
@@ -475,11 +488,17 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
             hh[4 * q + 3] = v.w;
         }
         const int given = kInit == kInitGiven ? (int)a.init[(uint64_t)r * a.ldi + i] : 0;
-        int code;
+        int code, shift;
         uint2 best_p;
-        search_group<kInit>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p);
+        float e_best, e_init;
+        search_group<kInit, kStats>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p, shift, e_best, e_init);
         a.codes[(uint64_t)r * a.ldc + i] = (uint8_t)code;
         a.packed[(uint64_t)r * a.ldp_vec + i] = best_p;
+        if (kStats) {
+            a.shift[g] = (int8_t)shift;
+            a.err_best[g] = e_best;
+            a.err_init[g] = e_init;
+        }
 
         if (a.num_groups - g <= stride) break;
         g += stride;
@@ -505,6 +524,154 @@ __global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *_
         load_group(W, g, w);
         const int c = min(max((int)codes[g], 1), kMaxCode);
         packed[g] = quantize_group(w, tab[c + kTabPad].R, make_uint2(0u, 0u));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Selected-shift statistics (the paper's appendix on selected scale shifts):
+// per shift d, the number of groups that chose it and the fp64 sums of their
+// initial errors, chosen errors and relative reductions.  Deterministic: each
+// block reduces a fixed chunk in a fixed order, then one wave per bin sums
+// the block partials in a fixed order.
+// ---------------------------------------------------------------------------
+
+constexpr int kSumThreads = 256;
+constexpr int kSumPerThread = 16;
+constexpr int kSumChunk = kSumThreads * kSumPerThread;
+constexpr int kSumOutside = 1 << 20;  // shift value standing for "no group"
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// Block b reduces groups [b * kSumChunk, (b + 1) * kSumChunk) into
+// part[(b * K + k) * 3 + {0: init, 1: best, 2: rel}] and cnt[b * K + k] for
+// every bin k = d + down (zeros for bins no group of the chunk chose).
+__global__ __launch_bounds__(kSumThreads) void shift_summary_partial(const int8_t *__restrict__ shift,
+                                                                     const float *__restrict__ err_best,
+                                                                     const float *__restrict__ err_init,
+                                                                     int64_t groups, int down, int up,
+                                                                     double *__restrict__ part,
+                                                                     uint32_t *__restrict__ cnt) {
+    __shared__ double red[kSumThreads / 64][3];
+    __shared__ uint32_t redc[kSumThreads / 64];
+    __shared__ int lim[2][kSumThreads / 64];
+    const int K = down + up + 1;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t base = (int64_t)blockIdx.x * kSumChunk;
+    int d[kSumPerThread];
+    float eb[kSumPerThread], ei[kSumPerThread];
+    int lo = kSumOutside, hi = -kSumOutside;
+#pragma unroll
+    for (int e = 0; e < kSumPerThread; ++e) {
+        const int64_t g = base + threadIdx.x + (int64_t)e * kSumThreads;
+        d[e] = kSumOutside;
+        eb[e] = ei[e] = 0.0f;
+        if (g < groups) {
+            const int v = shift[g];
+            if (v >= -down && v <= up) {
+                d[e] = v;
+                eb[e] = err_best[g];
+                ei[e] = err_init[g];
+                lo = min(lo, v);
+                hi = max(hi, v);
+            }
+        }
+    }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    if (lane == 0) {
+        lim[0][wave] = lo;
+        lim[1][wave] = hi;
+    }
+    __syncthreads();
+    lo = min(min(lim[0][0], lim[0][1]), min(lim[0][2], lim[0][3]));
+    hi = max(max(lim[1][0], lim[1][1]), max(lim[1][2], lim[1][3]));
+    double *bp = part + (size_t)blockIdx.x * K * 3;
+    uint32_t *bc = cnt + (size_t)blockIdx.x * K;
+    for (int k = threadIdx.x; k < K; k += kSumThreads) {
+        if (k - down < lo || k - down > hi) {
+            bp[3 * k] = bp[3 * k + 1] = bp[3 * k + 2] = 0.0;
+            bc[k] = 0u;
+        }
+    }
+    for (int v = lo; v <= hi; ++v) {  // block-uniform bounds
+        double si = 0.0, sb = 0.0, sr = 0.0;
+        uint32_t c = 0;
+#pragma unroll
+        for (int e = 0; e < kSumPerThread; ++e) {
+            if (d[e] == v) {
+                const double a = ei[e], b = eb[e];
+                ++c;
+                si += a;
+                sb += b;
+                sr += a > 0.0 ? (a - b) / a : 0.0;
+            }
+        }
+        si = wave_sum(si);
+        sb = wave_sum(sb);
+        sr = wave_sum(sr);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+        if (lane == 0) {
+            red[wave][0] = si;
+            red[wave][1] = sb;
+            red[wave][2] = sr;
+            redc[wave] = c;
+        }
+        __syncthreads();
+        if (threadIdx.x < 3) {
+            const int q = threadIdx.x;
+            bp[3 * (v + down) + q] = (red[0][q] + red[1][q]) + (red[2][q] + red[3][q]);
+        } else if (threadIdx.x == 3) {
+            bc[v + down] = (redc[0] + redc[1]) + (redc[2] + redc[3]);
+        }
+        __syncthreads();
+    }
+}
+
+// One wave per bin: lane l sums the partials of blocks l, l + 64, ... in
+// order, then a fixed butterfly combines the lanes.
+__global__ __launch_bounds__(64) void shift_summary_final(const double *__restrict__ part,
+                                                          const uint32_t *__restrict__ cnt, int64_t blocks,
+                                                          int K, uint64_t *__restrict__ count,
+                                                          double *__restrict__ sum_init,
+                                                          double *__restrict__ sum_best,
+                                                          double *__restrict__ sum_rel) {
+    const int k = blockIdx.x;
+    double si = 0.0, sb = 0.0, sr = 0.0;
+    uint64_t c = 0;
+    for (int64_t b = threadIdx.x; b < blocks; b += 64) {
+        const double *p = part + ((size_t)b * K + k) * 3;
+        si += p[0];
+        sb += p[1];
+        sr += p[2];
+        c += cnt[(size_t)b * K + k];
+    }
+    si = wave_sum(si);
+    sb = wave_sum(sb);
+    sr = wave_sum(sr);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (threadIdx.x == 0) {
+        count[k] = c;
+        sum_init[k] = si;
+        sum_best[k] = sb;
+        sum_rel[k] = sr;
     }
 }
 
@@ -553,7 +720,9 @@ size_t span(int64_t rows, int64_t ld, int64_t width, size_t elem) {
 
 int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
                  float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, uint8_t *codes, int64_t ldc,
-                 uint8_t *packed, int64_t ldp, hipStream_t stream) {
+                 uint8_t *packed, int64_t ldp, hipStream_t stream, int8_t *shift = nullptr,
+                 float *err_best = nullptr, float *err_init = nullptr) {
+    const bool stats = shift || err_best || err_init;
     if (out < 0 || cols < 0 || cols % kGroup != 0) return HSCALE_ERR_SHAPE;
     const int64_t Gc = cols / kGroup;
     if (out > 0 && cols > 0 && out > kMaxGroups / Gc) return HSCALE_ERR_SHAPE;
@@ -563,8 +732,10 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
     if (out == 0 || cols == 0) return HSCALE_OK;
     if (ldw < cols || ldc < Gc || ldp < cols / 2 || (init_mode == kInitGiven && ldi < Gc)) return HSCALE_ERR_SHAPE;
     if (!W || !h || !codes || !packed || (init_mode == kInitGiven && !init_codes)) return HSCALE_ERR_NULL;
+    if (stats && (!shift || !err_best || !err_init)) return HSCALE_ERR_NULL;
     if (!aligned(W, 16) || ldw % 8 != 0 || !aligned(h, 16) || !aligned(packed, 8) || ldp % 8 != 0)
         return HSCALE_ERR_ALIGN;
+    if (stats && (!aligned(err_best, 4) || !aligned(err_init, 4))) return HSCALE_ERR_ALIGN;
     const size_t nw = span(out, ldw, cols, 2), nh = (size_t)cols * 4;
     const size_t nc = span(out, ldc, Gc, 1), np = span(out, ldp, cols / 2, 1);
     if (overlaps(codes, nc, W, nw) || overlaps(codes, nc, h, nh) || overlaps(packed, np, W, nw) ||
@@ -576,6 +747,23 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
         const size_t ni = span(out, ldi, Gc, 1);
         const bool in_place = init_codes == codes && ldi == ldc;
         if ((!in_place && overlaps(init_codes, ni, codes, nc)) || overlaps(init_codes, ni, packed, np))
+            return HSCALE_ERR_OVERLAP;
+    }
+    if (stats) {
+        // Every statistics array is written: none may overlap another buffer.
+        const size_t groups = (size_t)out * (size_t)Gc;
+        const struct {
+            const void *p;
+            size_t n;
+        } in_bufs[] = {{W, nw}, {h, nh}, {codes, nc}, {packed, np},
+                       {init_codes, init_mode == kInitGiven ? span(out, ldi, Gc, 1) : 0}},
+          st[] = {{shift, groups}, {err_best, groups * 4}, {err_init, groups * 4}};
+        for (const auto &a : st) {
+            for (const auto &b : in_bufs)
+                if (b.n && overlaps(a.p, a.n, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+        }
+        if (overlaps(shift, groups, err_best, groups * 4) || overlaps(shift, groups, err_init, groups * 4) ||
+            overlaps(err_best, groups * 4, err_init, groups * 4))
             return HSCALE_ERR_OVERLAP;
     }
     SearchArgs a;
@@ -593,14 +781,31 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
     a.ldc = (uint64_t)ldc;
     a.packed = reinterpret_cast<uint2 *>(packed);
     a.ldp_vec = (uint64_t)ldp / 8;
+    a.shift = shift;
+    a.err_best = err_best;
+    a.err_init = err_init;
     const dim3 grid(grid_for(out * Gc)), block(kSearchThreads);
-    switch (init_mode) {
-        case kInitMaxAbs: hipLaunchKernelGGL(search_kernel<kInitMaxAbs>, grid, block, 0, stream, a); break;
-        case kInitFourOverSix: hipLaunchKernelGGL(search_kernel<kInitFourOverSix>, grid, block, 0, stream, a); break;
-        default: hipLaunchKernelGGL(search_kernel<kInitGiven>, grid, block, 0, stream, a); break;
+    if (!stats) {
+        switch (init_mode) {
+            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, false>), grid, block, 0, stream, a); break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, false>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, false>), grid, block, 0, stream, a); break;
+        }
+    } else {
+        switch (init_mode) {
+            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, true>), grid, block, 0, stream, a); break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, true>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, true>), grid, block, 0, stream, a); break;
+        }
     }
     return launch_status();
 }
+
+int64_t summary_blocks(int64_t groups) { return groups > 0 ? (groups + kSumChunk - 1) / kSumChunk : 0; }
 
 int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, void *workspace,
               size_t workspace_bytes, hipStream_t stream) {
@@ -716,6 +921,65 @@ int hscale_search_from(const void *W, int64_t out, int64_t in, const float *h, i
                        hipStream_t stream) {
     return search_block(W, in, out, in, h, down, up, global_scale, kInitGiven, init_codes, in / kGroup,
                         scale_codes, in / kGroup, packed_e2m1, in / 2, stream);
+}
+
+int hscale_search_stats(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                        float global_scale, int32_t init_mode, const uint8_t *init_codes, uint8_t *scale_codes,
+                        uint8_t *packed_e2m1, int8_t *shift, float *err_best, float *err_init, hipStream_t stream) {
+    if (out > 0 && in > 0 && (!shift || !err_best || !err_init)) return HSCALE_ERR_NULL;
+    return search_block(W, in, out, in, h, down, up, global_scale, init_mode, init_codes, in / kGroup, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream, shift, err_best, err_init);
+}
+
+size_t hscale_shift_summary_workspace_bytes(int64_t groups, int32_t down, int32_t up) {
+    if (groups <= 0 || down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow || groups > kMaxGroups) return 0;
+    const size_t K = (size_t)(down + up + 1);
+    return (size_t)summary_blocks(groups) * K * (3 * sizeof(double) + sizeof(uint32_t));
+}
+
+int hscale_shift_summary(const int8_t *shift, const float *err_best, const float *err_init, int64_t groups,
+                         int32_t down, int32_t up, uint64_t *count, double *sum_init, double *sum_best,
+                         double *sum_rel, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (groups < 0 || groups > kMaxGroups) return HSCALE_ERR_SHAPE;
+    if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
+    const int K = down + up + 1;
+    if (!count || !sum_init || !sum_best || !sum_rel) return HSCALE_ERR_NULL;
+    if (!aligned(count, 8) || !aligned(sum_init, 8) || !aligned(sum_best, 8) || !aligned(sum_rel, 8))
+        return HSCALE_ERR_ALIGN;
+    const size_t nk = (size_t)K * 8;
+    const void *outs[4] = {count, sum_init, sum_best, sum_rel};
+    for (int a = 0; a < 4; ++a)
+        for (int b = a + 1; b < 4; ++b)
+            if (overlaps(outs[a], nk, outs[b], nk)) return HSCALE_ERR_OVERLAP;
+    const int64_t blocks = summary_blocks(groups);
+    const size_t need = hscale_shift_summary_workspace_bytes(groups, down, up);
+    if (groups > 0) {
+        if (!shift || !err_best || !err_init) return HSCALE_ERR_NULL;
+        if (!aligned(err_best, 4) || !aligned(err_init, 4)) return HSCALE_ERR_ALIGN;
+        if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
+        if (!workspace) return HSCALE_ERR_NULL;
+        if (!aligned(workspace, 8)) return HSCALE_ERR_ALIGN;
+        const size_t g = (size_t)groups;
+        const struct {
+            const void *p;
+            size_t n;
+        } in_bufs[] = {{shift, g}, {err_best, g * 4}, {err_init, g * 4}, {workspace, need}};
+        for (int a = 0; a < 4; ++a)
+            for (const auto &b : in_bufs)
+                if (overlaps(outs[a], nk, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+        for (int a = 0; a < 3; ++a)
+            if (overlaps(workspace, need, in_bufs[a].p, in_bufs[a].n)) return HSCALE_ERR_OVERLAP;
+    }
+    double *part = static_cast<double *>(workspace);
+    uint32_t *cnt = blocks > 0 ? reinterpret_cast<uint32_t *>(part + (size_t)blocks * K * 3) : nullptr;
+    if (blocks > 0) {
+        hipLaunchKernelGGL(shift_summary_partial, dim3((unsigned)blocks), dim3(kSumThreads), 0, stream, shift,
+                           err_best, err_init, groups, down, up, part, cnt);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    }
+    hipLaunchKernelGGL(shift_summary_final, dim3((unsigned)K), dim3(64), 0, stream, part, cnt, blocks, K, count,
+                       sum_init, sum_best, sum_rel);
+    return launch_status();
 }
 
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,

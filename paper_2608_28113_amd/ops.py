@@ -178,3 +178,60 @@ def quantize(W: torch.Tensor, global_scale: float, scale_codes: torch.Tensor,
     _check(_lib.hscale_quantize(W.data_ptr(), m, n, float(global_scale), scale_codes.data_ptr(),
                                 packed_e2m1.data_ptr(), _stream(stream)), "hscale_quantize")
     return packed_e2m1
+
+
+def search_stats(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: int, up: int, init="maxabs",
+                 stream=None):
+    """The search with per-group statistics.  Returns a dict of
+    scale_codes, packed_e2m1, shift (int8 [out, in/16], the chosen shift),
+    err_best and err_init (fp32 [out, in/16], the score at the chosen shift
+    and at shift 0)."""
+    _bf16_matrix(W, "W")
+    m, n = W.shape
+    if h.dtype != torch.float32 or h.shape != (n,) or not h.is_contiguous():
+        raise ValueError("h must be a contiguous fp32 tensor of shape [in]")
+    mode, init_t = _init_mode(init)
+    iptr = 0
+    if init_t is not None:
+        if init_t.shape != (m, n // 16) or not init_t.is_contiguous():
+            raise ValueError("initial codes must be a contiguous uint8 tensor [out, in/16]")
+        iptr = init_t.data_ptr()
+    G = (m, n // 16)
+    out = dict(scale_codes=torch.empty(G, dtype=torch.uint8, device=W.device),
+               packed_e2m1=torch.empty((m, n // 2), dtype=torch.uint8, device=W.device),
+               shift=torch.empty(G, dtype=torch.int8, device=W.device),
+               err_best=torch.empty(G, dtype=torch.float32, device=W.device),
+               err_init=torch.empty(G, dtype=torch.float32, device=W.device))
+    st = _lib.hscale_search_stats(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale), mode,
+                                  iptr, out["scale_codes"].data_ptr(), out["packed_e2m1"].data_ptr(),
+                                  out["shift"].data_ptr(), out["err_best"].data_ptr(), out["err_init"].data_ptr(),
+                                  _stream(stream))
+    _check(st, "hscale_search_stats")
+    return out
+
+
+def shift_summary(shift: torch.Tensor, err_best: torch.Tensor, err_init: torch.Tensor, down: int, up: int,
+                  stream=None) -> dict:
+    """Per-shift counts and fp64 sums of initial errors, chosen errors and
+    relative reductions over the groups (bins d = -down..up), as tensors of
+    length down + up + 1 on the device."""
+    groups = shift.numel()
+    for t, dt, name in ((shift, torch.int8, "shift"), (err_best, torch.float32, "err_best"),
+                        (err_init, torch.float32, "err_init")):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous() or t.numel() != groups:
+            raise ValueError(f"{name} must be a contiguous {dt} CUDA tensor with one entry per group")
+    K = int(down) + int(up) + 1
+    dev = shift.device
+    # counts are uint64 in the C ABI; int64 holds them (< 2^63) with full torch support
+    out = dict(count=torch.empty(K, dtype=torch.int64, device=dev),
+               sum_init=torch.empty(K, dtype=torch.float64, device=dev),
+               sum_best=torch.empty(K, dtype=torch.float64, device=dev),
+               sum_rel=torch.empty(K, dtype=torch.float64, device=dev))
+    need = _lib.hscale_shift_summary_workspace_bytes(groups, int(down), int(up))
+    ws = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
+    st = _lib.hscale_shift_summary(shift.data_ptr(), err_best.data_ptr(), err_init.data_ptr(), groups, int(down),
+                                   int(up), out["count"].data_ptr(), out["sum_init"].data_ptr(),
+                                   out["sum_best"].data_ptr(), out["sum_rel"].data_ptr(), ws.data_ptr(), need,
+                                   _stream(stream))
+    _check(st, "hscale_shift_summary")
+    return out

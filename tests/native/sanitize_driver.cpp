@@ -18,6 +18,14 @@ void oracle_hdiag(const uint16_t *X, int64_t tokens, int64_t n, double *h);
 int oracle_quantize(const uint16_t *W, int64_t m, int64_t n, float s_g, const uint8_t *codes, const float *h,
                     uint8_t *packed, double *err);
 int oracle_all_code_errors(const uint16_t *W, int64_t m, int64_t n, const float *h, float s_g, double *err);
+int oracle_search_stats(const uint16_t *W, int64_t m, int64_t n, const float *h, int down, int up, float s_g,
+                        int init_mode, const uint8_t *init_codes, uint8_t *codes, uint8_t *packed, double *e_best,
+                        double *e_second, uint8_t *c0, double *l4, double *l6, int8_t *shift, double *e_init);
+int oracle_delta(const uint16_t *W, int64_t m, int64_t n, float s_g, const uint8_t *codes, const uint8_t *packed,
+                 double *delta);
+int oracle_output_error(const uint16_t *X, int64_t T, int64_t n, const double *delta, int64_t m, double *row_err);
+int oracle_shift_summary(const int8_t *shift, const double *e_best, const double *e_init, int64_t groups, int down,
+                         int up, int64_t *count, double *sum_init, double *sum_best, double *sum_rel);
 }
 
 static uint16_t bf16(float f) {
@@ -47,6 +55,15 @@ int main() {
     bad |= oracle_all_code_errors(W.data(), m, n, h.data(), 1e-4f, all.data()) != 0;
     bad |= oracle_search_init(W.data(), m, 15, h.data(), 4, 4, 1e-4f, 0, nullptr, codes.data(), packed.data(),
                               nullptr, nullptr, nullptr, nullptr, nullptr) != -1;
+    std::vector<int8_t> shift(m * G);
+    std::vector<double> ei(m * G), delta(m * n), row(m, 0.0), si(16), sb(16), sr(16);
+    std::vector<int64_t> cnt(16);
+    bad |= oracle_search_stats(W.data(), m, n, h.data(), 9, 6, 1e-4f, 0, nullptr, codes.data(), packed.data(),
+                               eb.data(), es.data(), c0.data(), l4.data(), l6.data(), shift.data(), ei.data()) != 0;
+    bad |= oracle_delta(W.data(), m, n, 1e-4f, codes.data(), packed.data(), delta.data()) != 0;
+    bad |= oracle_output_error(X.data(), T, n, delta.data(), m, row.data()) != 0;
+    bad |= oracle_shift_summary(shift.data(), eb.data(), ei.data(), m * G, 9, 6, cnt.data(), si.data(), sb.data(),
+                                sr.data()) != 0;
 
     // Library validation: fake, aligned addresses; every call must be rejected
     // (or be empty) before any launch.
@@ -65,6 +82,13 @@ int main() {
                               (uint8_t *)(A + 12288), nullptr) != HSCALE_ERR_NULL;
     bad |= hscale_quantize(A, 0, 64, 1e-3f, nullptr, nullptr, nullptr) != HSCALE_OK;
     bad |= hscale_hdiag_finalize(nullptr, 0, nullptr, nullptr) != HSCALE_OK;
+    bad |= hscale_search_stats(A, 4, 64, (float *)(A + 4096), 4, 4, 1e-3f, 0, nullptr, (uint8_t *)(A + 8192),
+                               (uint8_t *)(A + 12288), (int8_t *)(A + 16384), (float *)(A + 16386),
+                               (float *)(A + 20480), nullptr) != HSCALE_ERR_ALIGN;
+    bad |= hscale_shift_summary_workspace_bytes(5000, 9, 6) == 0;
+    bad |= hscale_shift_summary((int8_t *)A, (float *)(A + 4096), (float *)(A + 8192), 1000, 9, 6,
+                                (uint64_t *)(A + 12288), (double *)(A + 12296), (double *)(A + 16384),
+                                (double *)(A + 20480), A + 24576, 1 << 20, nullptr) != HSCALE_ERR_OVERLAP;
     for (int s = -9; s <= 1; ++s) bad |= hscale_status_string(s) == nullptr;
     std::printf(bad ? "sanitize driver: FAILED\n" : "sanitize driver: ok\n");
     return bad;

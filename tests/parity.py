@@ -20,6 +20,13 @@ H_REL_TOL = 1e-5
 TIE_REL = oracle.NEAR_TIE_REL
 
 
+def oracle_h32(X_bits: np.ndarray) -> np.ndarray:
+    """h for a search parity case, computed by the oracle from the seeded X
+    and rounded to fp32; the HIP search and the oracle search both take it
+    as input (no oracle input comes from the HIP path)."""
+    return oracle.hdiag(X_bits).astype(np.float32)
+
+
 def compare_h(h_gpu: np.ndarray, h_ref: np.ndarray) -> dict:
     h_gpu = np.asarray(h_gpu, np.float64)
     zero = h_ref == 0
@@ -75,4 +82,47 @@ def compare_search(W_bits: np.ndarray, h32: np.ndarray, s_g: float, down: int, u
         invalid=int((~valid).sum()),
         ok=bool(strict_bad.sum() == 0 and packed_consistent.all() and valid.all()),
         oracle=r,
+        tie_mask=tie | init_tie,
+        init_tie_mask=init_tie,
+        err_at_gpu_codes=err_at,
     )
+
+
+# fp32 score of one group against the fp64 oracle: each of the 16 positive
+# terms carries a few roundings (residual, square, weight) and the sum runs
+# 4 chains of 4 then a 2-level tree, about 10 units of 2^-24 in all; the
+# bound below leaves a factor of 3.
+ERR_REL_TOL = 2e-6
+
+
+def compare_stats(W_bits: np.ndarray, h32: np.ndarray, s_g: float, down: int, up: int, gpu: dict,
+                  init="rtn") -> dict:
+    """hscale_search_stats' outputs against the oracle: the search outputs as
+    compare_search; the chosen shift bit-exact outside near-ties (and in
+    range, consistent with the code, for every group); err_best within
+    ERR_REL_TOL of the oracle's error at the GPU's code; err_init within
+    ERR_REL_TOL of the oracle's error at the initial code."""
+    m, n = W_bits.shape
+    G = n // 16
+    rep = compare_search(W_bits, h32, s_g, down, up, gpu["scale_codes"], gpu["packed_e2m1"], init=init)
+    r = rep["oracle"]
+    skip = rep["tie_mask"]
+    shift = np.asarray(gpu["shift"], np.int64).reshape(m, G)
+    eb = np.asarray(gpu["err_best"], np.float64).reshape(m, G)
+    ei = np.asarray(gpu["err_init"], np.float64).reshape(m, G)
+    codes = np.asarray(gpu["scale_codes"], np.int64).reshape(m, G)
+    in_range = (shift >= -down) & (shift <= up)
+    c0 = r["c0"].astype(np.int64)
+    consistent = (np.clip(c0 + shift, 1, 126) == codes) | rep["init_tie_mask"]
+    shift_bad = (shift != r["shift"]) & ~skip
+
+    def rel(a, b):
+        return np.abs(a - b) / np.where(b > 0, b, 1.0)
+
+    eb_rel = rel(eb, rep["err_at_gpu_codes"])
+    ei_rel = np.where(rep["init_tie_mask"], 0.0, rel(ei, r["e_init"]))
+    ok = (rep["ok"] and in_range.all() and consistent.all() and shift_bad.sum() == 0
+          and eb_rel.max(initial=0) <= ERR_REL_TOL and ei_rel.max(initial=0) <= ERR_REL_TOL)
+    return dict(search=rep, shift_mismatches=int(shift_bad.sum()), shift_out_of_range=int((~in_range).sum()),
+                shift_inconsistent=int((~consistent).sum()), err_best_max_rel=float(eb_rel.max(initial=0)),
+                err_init_max_rel=float(ei_rel.max(initial=0)), ok=bool(ok))

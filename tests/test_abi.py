@@ -170,3 +170,52 @@ def test_variant_validation(L):
     assert L.hscale_hdiag_finalize(h64, 33, h, 0) == -2
     assert L.hscale_hdiag_finalize(h64, 32, h64 + 64, 0) == -8
     assert L.hscale_hdiag_finalize(0, 0, 0, 0) == 0
+
+
+def test_stats_and_summary_validation(L):
+    m, n = 4, 64
+    W, h, codes, packed, sh, eb, ei = A, 2 * A, 3 * A, 4 * A, 5 * A, 6 * A, 7 * A
+
+    def st(**k):
+        return L.hscale_search_stats(W, m, n, h, 4, 4, 1e-3, k.get("mode", 0), k.get("init", 0), codes, packed,
+                                     k.get("sh", sh), k.get("eb", eb), k.get("ei", ei), 0)
+    # every call fails validation: nothing is launched on the fake addresses
+    assert st(sh=0) == -1
+    assert st(eb=0) == -1
+    assert st(ei=0) == -1
+    assert st(eb=eb + 2) == -3
+    assert st(mode=2) == -1
+    assert st(ei=eb + 8) == -8          # err arrays overlap
+    assert st(sh=W + 16) == -8          # statistics overlap W
+    assert st(eb=codes) == -8           # statistics overlap the codes
+    assert L.hscale_search_stats(W, m, n, h, 126, 4, 1e-3, 0, 0, codes, packed, sh, eb, ei, 0) == -4
+
+    assert L.hscale_shift_summary_workspace_bytes(0, 4, 4) == 0
+    assert L.hscale_shift_summary_workspace_bytes(-5, 4, 4) == 0
+    assert L.hscale_shift_summary_workspace_bytes(10, -1, 4) == 0
+    b1 = L.hscale_shift_summary_workspace_bytes(1, 4, 4)
+    b2 = L.hscale_shift_summary_workspace_bytes(4097, 4, 4)
+    assert b1 > 0 and b2 == 2 * b1 and L.hscale_shift_summary_workspace_bytes(1, 9, 6) > b1
+
+    cnt, si, sb, sr, ws = 8 * A, 9 * A, 10 * A, 11 * A, 12 * A
+    need = L.hscale_shift_summary_workspace_bytes(1000, 4, 4)
+
+    def su(groups=1000, down=4, up=4, **k):
+        return L.hscale_shift_summary(k.get("sh", sh), k.get("eb", eb), k.get("ei", ei), groups, down, up,
+                                      k.get("cnt", cnt), k.get("si", si), k.get("sb", sb), k.get("sr", sr),
+                                      k.get("ws", ws), k.get("wsb", need), 0)
+    assert su(groups=-1) == -2
+    assert su(groups=1 << 33) == -2
+    assert su(down=-1) == -4
+    assert su(up=126) == -4
+    assert su(cnt=0) == -1
+    assert su(sr=0) == -1
+    assert su(sh=0) == -1
+    assert su(ws=0) == -1
+    assert su(wsb=need - 1) == -6
+    assert su(cnt=cnt + 4) == -3
+    assert su(eb=eb + 2) == -3
+    assert su(ws=ws + 4) == -3
+    assert su(si=cnt + 8) == -8         # outputs overlap
+    assert su(sb=eb) == -8              # output overlaps an input
+    assert su(ws=sh) == -8              # workspace overlaps an input

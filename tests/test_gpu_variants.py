@@ -29,8 +29,7 @@ def hs():
 def tiny(hs):
     wl = CONFIGS["tiny"]
     W = make_weight(wl, "cpu")
-    h = hs.hdiag(make_activations(wl, "cpu").to(DEV))
-    torch.cuda.synchronize()
+    h = torch.from_numpy(parity.oracle_h32(tensor_bits(make_activations(wl, "cpu")))).to(DEV)
     return W.to(DEV), h, harness_global_scale(W)
 
 
@@ -62,9 +61,7 @@ def test_4over6_window0_is_the_4over6_quantizer(hs, tiny):
 
 def test_4over6_full_size_sampled(hs):
     wl = CONFIGS["down_proj"]
-    X = make_activations(wl, DEV, tokens=32768)
-    h = hs.hdiag(X)
-    del X
+    h = torch.from_numpy(parity.oracle_h32(tensor_bits(make_activations(wl, "cpu", tokens=4096)))).to(DEV)
     W = make_weight(wl, DEV)
     s_g = harness_global_scale(W)
     codes, packed = hs.search(W, h, s_g, down=9, up=6, init="4over6")
