@@ -19,7 +19,8 @@
  * GPTQ-style blockwise use, and h accumulated over streamed calibration
  * batches.  Quality diagnostics of the appendix: the search with per-group
  * statistics (chosen shift, its error, the error at shift 0) and their
- * per-shift summary.
+ * per-shift summary, and the layer-output error of Eq. 3 by which the
+ * appendix scores a candidate window.
  *
  * Conventions shared by every entry point
  *   - All pointers are device pointers (hipMalloc'd or torch CUDA tensors)
@@ -267,6 +268,48 @@ int hscale_shift_summary(const int8_t *shift, const float *err_best,
                          int32_t up, uint64_t *count, double *sum_init,
                          double *sum_best, double *sum_rel, void *workspace,
                          size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes hscale_output_error needs (0 when any size is 0). */
+size_t hscale_output_error_workspace_bytes(int64_t tokens, int64_t in,
+                                           int64_t out);
+
+/*
+ * Layer-output error of a stored NVFP4 tensor on calibration activations
+ * (Sec. 3.2, Eq. 3; the L_full by which the appendix's window sweep scores
+ * chosen scales), split by output row:
+ *
+ *   row_err[r] += sum_t ( sum_j X[t, j] * dW[r, j] )^2,
+ *   dW[r, j] = W[r, j] - v[r, j] * S[c]
+ *
+ * where c is the group's scale code, v the signed E2M1 value of its nibble
+ * and S[c] = fp32(global_scale * l_c) (S[0] = 0).  The layer's
+ * ||X dW^T||_F^2 = Tr(dW X^T X dW^T) is the sum of row_err.  row_err is
+ * accumulated into, so calibration batches streamed through successive
+ * calls add up; zero it first.
+ *
+ * Arithmetic: dW is formed in fp32 with one rounding and split into two bf16
+ * parts hi + lo (within 2^-18 |dW|); X dW^T is computed on the matrix cores
+ * as bf16 products accumulated in fp32; squares and sums are fp64 in a fixed
+ * order (bitwise reproducible for a given problem).
+ *
+ * X            bf16 [tokens, in], 16-byte aligned
+ * W            bf16 [out, in], 16-byte aligned
+ * scale_codes  uint8 [out, in / 16], E4M3FN codes 0..126 (other bytes give
+ *              unspecified results)
+ * packed_e2m1  uint8 [out, in / 2], 8-byte aligned, element 2k in the low
+ *              nibble of byte k
+ * row_err      fp64 [out], 8-byte aligned, in/out
+ * workspace    >= hscale_output_error_workspace_bytes(tokens, in, out)
+ *              bytes, 256-byte aligned, scratch owned by the caller (it holds
+ *              the two dW planes and per-tile partial sums)
+ * in % 16 == 0; global_scale as hscale_search.  tokens, in or out = 0 adds
+ * nothing.
+ */
+int hscale_output_error(const void *X, int64_t tokens, int64_t in,
+                        const void *W, int64_t out, float global_scale,
+                        const uint8_t *scale_codes, const uint8_t *packed_e2m1,
+                        double *row_err, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Final re-quantization at given scale codes (Sec. 3.3; Eq. 12 at a fixed

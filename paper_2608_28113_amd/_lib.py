@@ -32,6 +32,8 @@ EXPORTS = (
     "hscale_search_stats",
     "hscale_shift_summary_workspace_bytes",
     "hscale_shift_summary",
+    "hscale_output_error_workspace_bytes",
+    "hscale_output_error",
     "hscale_quantize",
 )
 
@@ -84,6 +86,10 @@ def load() -> ctypes.CDLL:
     lib.hscale_shift_summary_workspace_bytes.restype = sz
     lib.hscale_shift_summary.argtypes = [P, P, P, i64, i32, i32, P, P, P, P, P, sz, P]
     lib.hscale_shift_summary.restype = ctypes.c_int
+    lib.hscale_output_error_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.hscale_output_error_workspace_bytes.restype = sz
+    lib.hscale_output_error.argtypes = [P, i64, i64, P, i64, f32, P, P, P, P, sz, P]
+    lib.hscale_output_error.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -169,3 +175,14 @@ def hscale_shift_summary(shift: int, err_best: int, err_init: int, groups: int, 
     return load().hscale_shift_summary(shift or None, err_best or None, err_init or None, groups, down, up,
                                        count or None, sum_init or None, sum_best or None, sum_rel or None,
                                        workspace or None, workspace_bytes, stream or None)
+
+
+def hscale_output_error_workspace_bytes(tokens: int, in_: int, out: int) -> int:
+    return load().hscale_output_error_workspace_bytes(tokens, in_, out)
+
+
+def hscale_output_error(X: int, tokens: int, in_: int, W: int, out: int, global_scale: float, scale_codes: int,
+                        packed_e2m1: int, row_err: int, workspace: int, workspace_bytes: int, stream: int) -> int:
+    return load().hscale_output_error(X or None, tokens, in_, W or None, out, global_scale, scale_codes or None,
+                                      packed_e2m1 or None, row_err or None, workspace or None, workspace_bytes,
+                                      stream or None)

@@ -676,6 +676,213 @@ __global__ __launch_bounds__(64) void shift_summary_final(const double *__restri
 }
 
 // ---------------------------------------------------------------------------
+// Layer-output error (Sec. 3.2, Eq. 3): L_r = sum_t (X dW^T)_tr^2 per output
+// row r, with dW = W - W^ the rounding error of a stored NVFP4 tensor.
+//
+// dW is formed once in fp32 (w - v S[c], one rounding) and split into two
+// bf16 planes hi + lo (|dW - hi - lo| <= 2^-18 |dW|), so X dW^T is two bf16
+// MFMA products accumulated in fp32.  Each block computes a 256-token x
+// 128-row tile of X dW^T in registers and reduces the squares of its columns
+// in fp64; the tile is never written.  Per-tile column sums go to a
+// workspace and a fixed-order tree adds them to row_err.
+// ---------------------------------------------------------------------------
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kLfBM = 256;  // tokens per tile
+constexpr int kLfBN = 128;  // weight rows per tile
+constexpr int kLfBK = 32;   // k per LDS stage (two 16-deep MFMA steps)
+constexpr int kLfThreads = 256;
+constexpr int64_t kLfMaxTilesPerPass = 1024;  // token tiles per tile launch (bounds the workspace)
+
+__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;  // finite inputs
+}
+
+// dW of one 16-weight group, split into hi / lo bf16 planes of row stride
+// ldd; groups beyond (out, in) in the padded planes are written as zeros.
+__global__ __launch_bounds__(256) void delta_split_kernel(const u32x4 *__restrict__ W, int64_t out, int64_t in,
+                                                          float s_g, const uint8_t *__restrict__ codes,
+                                                          const uint2 *__restrict__ packed, int64_t rows_pad,
+                                                          int64_t ldd, u32x4 *__restrict__ hi,
+                                                          u32x4 *__restrict__ lo) {
+    const int64_t Gp = ldd / kGroup, Gc = in / kGroup;
+    const int64_t total = rows_pad * Gp;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total; q += stride) {
+        const int64_t r = q / Gp, i = q % Gp;
+        uint32_t hb[8], lb[8];
+        if (r < out && i < Gc) {
+            const int64_t g = r * Gc + i;
+            float w[kGroup];
+            load_group(W, g, w);
+            const float S = s_g * e4m3fn_value(codes[g]);
+            const uint2 p = packed[g];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const uint32_t src = k < 4 ? p.x : p.y;
+                float2 v;
+                switch (k & 3) {
+                    case 0: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 0); v = make_float2(t[0], t[1]); break; }
+                    case 1: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 1); v = make_float2(t[0], t[1]); break; }
+                    case 2: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 2); v = make_float2(t[0], t[1]); break; }
+                    default: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 3); v = make_float2(t[0], t[1]); break; }
+                }
+                const float d0 = fmaf(-v.x, S, w[2 * k]);
+                const float d1 = fmaf(-v.y, S, w[2 * k + 1]);
+                const uint32_t h0 = bf16_bits_rne(d0), h1 = bf16_bits_rne(d1);
+                const uint32_t l0 = bf16_bits_rne(d0 - __uint_as_float(h0 << 16));
+                const uint32_t l1 = bf16_bits_rne(d1 - __uint_as_float(h1 << 16));
+                hb[k] = h0 | (h1 << 16);
+                lb[k] = l0 | (l1 << 16);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) hb[k] = lb[k] = 0u;
+        }
+        u32x4 *dh = hi + (r * ldd + i * kGroup) / 8;
+        u32x4 *dl = lo + (r * ldd + i * kGroup) / 8;
+        dh[0] = u32x4{hb[0], hb[1], hb[2], hb[3]};
+        dh[1] = u32x4{hb[4], hb[5], hb[6], hb[7]};
+        dl[0] = u32x4{lb[0], lb[1], lb[2], lb[3]};
+        dl[1] = u32x4{lb[4], lb[5], lb[6], lb[7]};
+    }
+}
+
+// LDS tiles hold rows of kLfBK bf16 (64 bytes = four 16-byte chunks); chunk c
+// of row r lives at chunk position c ^ ((r >> 1) & 3) so that the 32 rows an
+// MFMA operand read touches spread over the banks.
+__device__ __forceinline__ int lf_lds_offset(int row, int chunk) {
+    return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4);
+}
+
+struct LfArgs {
+    const u32x4 *X;      // [tokens, in] bf16
+    int64_t tokens, in;  // of this pass
+    const u32x4 *hi;     // [rows_pad, ldd] bf16 planes
+    const u32x4 *lo;
+    int64_t ldd;
+    int64_t out;           // weight rows
+    int64_t ntiles;        // rows_pad / kLfBN
+    double *partial;       // [token tiles of the pass, out]
+};
+
+__global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[2][(kLfBM + 2 * kLfBN) * 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int64_t mt = blockIdx.x / a.ntiles, nt = blockIdx.x % a.ntiles;
+    const int64_t t0 = mt * kLfBM, r0 = nt * kLfBN;
+    const int64_t xrow_vec = a.in / 8, drow_vec = a.ldd / 8;
+    const int stages = (int)((a.ldd) / kLfBK);
+
+    // Global -> register staging: 4 A chunks and 2 + 2 B chunks per thread.
+    u32x4 sa[4], sh[2], sl[2];
+    auto load_stage = [&](int s) {
+        const int64_t kvec = (int64_t)s * (kLfBK / 8);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
+            const int64_t t = t0 + row, kv = kvec + c;
+            sa[i] = (t < a.tokens && kv < xrow_vec) ? __builtin_nontemporal_load(a.X + t * xrow_vec + kv)
+                                                    : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
+            const int64_t off = (r0 + row) * drow_vec + kvec + c;
+            sh[i] = a.hi[off];
+            sl[i] = a.lo[off];
+        }
+    };
+    auto store_stage = [&](int buf) {
+        uint8_t *base = lds[buf];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
+            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(row, c)) = sa[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
+            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(kLfBM + row, c)) = sh[i];
+            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(kLfBM + kLfBN + row, c)) = sl[i];
+        }
+    };
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+    for (int s = 0; s < stages; ++s) {
+        const bool more = s + 1 < stages;
+        if (more) load_stage(s + 1);
+        const uint8_t *base = lds[s & 1];
+#pragma unroll
+        for (int kk = 0; kk < kLfBK / 16; ++kk) {
+            const int c = 2 * kk + (lane >> 5);
+            bf16x8 fa[4], fh[2], fl[2];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = wm * 128 + i * 32 + (lane & 31);
+                fa[i] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(row, c));
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int row = wn * 64 + j * 32 + (lane & 31);
+                fh[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + row, c));
+                fl[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + kLfBN + row, c));
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fl[j], acc[i][j], 0, 0, 0);
+                }
+        }
+        if (more) store_stage((s + 1) & 1);
+        __syncthreads();
+    }
+
+    // Column sums of squares: lane l holds column l % 32 of each 32x32
+    // accumulator; lanes l and l + 32 share a column, and waves wm = 0, 1
+    // share the wave's 64 columns.
+    double sq[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        double v = 0.0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const double y = (double)acc[i][j][e];
+                v = fma(y, y, v);
+            }
+        sq[j] = v + __shfl_xor(v, 32, 64);
+    }
+    double *red = reinterpret_cast<double *>(lds[0]);  // [2 wm][128 columns]
+    if (lane < 32) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) red[wm * kLfBN + wn * 64 + j * 32 + lane] = sq[j];
+    }
+    __syncthreads();
+    if (tid < kLfBN) {
+        const int64_t col = r0 + tid;
+        if (col < a.out) a.partial[mt * a.out + col] = red[tid] + red[kLfBN + tid];
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Host side: validation and launch
 // ---------------------------------------------------------------------------
 
@@ -803,6 +1010,27 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
         }
     }
     return launch_status();
+}
+
+struct LfPlan {
+    int64_t ldd = 0, rows_pad = 0, ntiles = 0, tiles_per_pass = 0;
+    size_t plane_bytes = 0, partial_offset = 0, bytes = 0;
+};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
+    LfPlan p;
+    if (tokens <= 0 || in <= 0 || out <= 0) return p;
+    p.ldd = (in + kLfBK - 1) / kLfBK * kLfBK;
+    p.rows_pad = (out + kLfBN - 1) / kLfBN * kLfBN;
+    p.ntiles = p.rows_pad / kLfBN;
+    const int64_t tiles = (tokens + kLfBM - 1) / kLfBM;
+    p.tiles_per_pass = tiles < kLfMaxTilesPerPass ? tiles : kLfMaxTilesPerPass;
+    p.plane_bytes = round_up((size_t)p.rows_pad * (size_t)p.ldd * 2, 256);
+    p.partial_offset = 2 * p.plane_bytes;
+    p.bytes = p.partial_offset + (size_t)p.tiles_per_pass * (size_t)out * sizeof(double);
+    return p;
 }
 
 int64_t summary_blocks(int64_t groups) { return groups > 0 ? (groups + kSumChunk - 1) / kSumChunk : 0; }
@@ -980,6 +1208,66 @@ int hscale_shift_summary(const int8_t *shift, const float *err_best, const float
     hipLaunchKernelGGL(shift_summary_final, dim3((unsigned)K), dim3(64), 0, stream, part, cnt, blocks, K, count,
                        sum_init, sum_best, sum_rel);
     return launch_status();
+}
+
+size_t hscale_output_error_workspace_bytes(int64_t tokens, int64_t in, int64_t out) {
+    if (in % kGroup != 0 || in > ((int64_t)1 << 40) || (in > 0 && out > kMaxGroups / (in / kGroup))) return 0;
+    return lfull_plan(tokens, in, out).bytes;
+}
+
+int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W, int64_t out, float global_scale,
+                        const uint8_t *scale_codes, const uint8_t *packed_e2m1, double *row_err, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+    if (tokens < 0 || in < 0 || out < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    if (in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+    if (!scale_ok(global_scale)) return HSCALE_ERR_SCALE;
+    if (tokens == 0 || in == 0 || out == 0) return HSCALE_OK;  // adds nothing
+    if (!X || !W || !scale_codes || !packed_e2m1 || !row_err || !workspace) return HSCALE_ERR_NULL;
+    if (!aligned(X, 16) || !aligned(W, 16) || !aligned(packed_e2m1, 8) || !aligned(row_err, 8) ||
+        !aligned(workspace, 256))
+        return HSCALE_ERR_ALIGN;
+    const LfPlan p = lfull_plan(tokens, in, out);
+    if (workspace_bytes < p.bytes) return HSCALE_ERR_WORKSPACE;
+    const size_t nx = (size_t)tokens * (size_t)in * 2, nw = (size_t)out * (size_t)in * 2;
+    const size_t nc = (size_t)out * (size_t)(in / kGroup), np = (size_t)out * (size_t)(in / 2);
+    const size_t nr = (size_t)out * 8;
+    const struct {
+        const void *p;
+        size_t n;
+    } ins[] = {{X, nx}, {W, nw}, {scale_codes, nc}, {packed_e2m1, np}};
+    for (const auto &b : ins)
+        if (overlaps(row_err, nr, b.p, b.n) || overlaps(workspace, p.bytes, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+    if (overlaps(row_err, nr, workspace, p.bytes)) return HSCALE_ERR_OVERLAP;
+
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    u32x4 *hi = reinterpret_cast<u32x4 *>(ws), *lo = reinterpret_cast<u32x4 *>(ws + p.plane_bytes);
+    double *partial = reinterpret_cast<double *>(ws + p.partial_offset);
+    hipLaunchKernelGGL(delta_split_kernel, dim3(grid_for(p.rows_pad * (p.ldd / kGroup))), dim3(256), 0, stream,
+                       static_cast<const u32x4 *>(W), out, in, global_scale, scale_codes,
+                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo);
+    if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    const int64_t pass_tokens = p.tiles_per_pass * kLfBM;
+    const unsigned tree_blocks = (unsigned)((out + kTreeCols - 1) / kTreeCols);
+    for (int64_t t0 = 0; t0 < tokens; t0 += pass_tokens) {
+        LfArgs a;
+        a.tokens = tokens - t0 < pass_tokens ? tokens - t0 : pass_tokens;
+        a.in = in;
+        a.X = static_cast<const u32x4 *>(X) + t0 * (in / 8);
+        a.hi = hi;
+        a.lo = lo;
+        a.ldd = p.ldd;
+        a.out = out;
+        a.ntiles = p.ntiles;
+        a.partial = partial;
+        const int64_t tiles = (a.tokens + kLfBM - 1) / kLfBM;
+        hipLaunchKernelGGL(lfull_tile_kernel, dim3((unsigned)(tiles * p.ntiles)), dim3(kLfThreads), 0, stream, a);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+        hipLaunchKernelGGL(hdiag_tree<true>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
+                           static_cast<const double *>(partial), tiles, out, (float *)nullptr, row_err);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    }
+    return HSCALE_OK;
 }
 
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,

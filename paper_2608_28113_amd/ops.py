@@ -235,3 +235,40 @@ def shift_summary(shift: torch.Tensor, err_best: torch.Tensor, err_init: torch.T
                                    _stream(stream))
     _check(st, "hscale_shift_summary")
     return out
+
+
+def output_error_workspace_bytes(tokens: int, in_features: int, out_features: int) -> int:
+    """Bytes of scratch output_error needs."""
+    return _lib.hscale_output_error_workspace_bytes(tokens, in_features, out_features)
+
+
+def output_error(X: torch.Tensor, W: torch.Tensor, global_scale: float, scale_codes: torch.Tensor,
+                 packed_e2m1: torch.Tensor, row_err: torch.Tensor | None = None,
+                 workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Eq. 3 per output row: row_err[r] += sum_t (X dW^T)_tr^2 with dW = W - W^
+    the rounding error of the stored NVFP4 tensor (scale_codes, packed_e2m1).
+    row_err is fp64 [out] (zeros when not given); the layer's L_full is its
+    sum."""
+    _bf16_matrix(X, "X")
+    _bf16_matrix(W, "W")
+    T, n = X.shape
+    m = W.shape[0]
+    if W.shape[1] != n:
+        raise ValueError("X and W disagree on in_features")
+    if scale_codes.dtype != torch.uint8 or scale_codes.shape != (m, n // 16) or not scale_codes.is_contiguous():
+        raise ValueError("scale_codes must be a contiguous uint8 tensor [out, in/16]")
+    if packed_e2m1.dtype != torch.uint8 or packed_e2m1.shape != (m, n // 2) or not packed_e2m1.is_contiguous():
+        raise ValueError("packed_e2m1 must be a contiguous uint8 tensor [out, in/2]")
+    if row_err is None:
+        row_err = torch.zeros(m, dtype=torch.float64, device=X.device)
+    if row_err.dtype != torch.float64 or row_err.shape != (m,) or not row_err.is_contiguous():
+        raise ValueError("row_err must be a contiguous fp64 tensor [out]")
+    need = output_error_workspace_bytes(T, n, m)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.hscale_output_error(X.data_ptr(), T, n, W.data_ptr(), m, float(global_scale),
+                                    scale_codes.data_ptr(), packed_e2m1.data_ptr(), row_err.data_ptr(), ws_ptr,
+                                    ws_bytes, _stream(stream)), "hscale_output_error")
+    return row_err

@@ -219,3 +219,39 @@ def test_stats_and_summary_validation(L):
     assert su(si=cnt + 8) == -8         # outputs overlap
     assert su(sb=eb) == -8              # output overlaps an input
     assert su(ws=sh) == -8              # workspace overlaps an input
+
+
+def test_output_error_validation(L):
+    T, n, m = 64, 64, 8
+    X, W, codes, packed, row, ws = A, 2 * A, 3 * A, 4 * A, 5 * A, 6 * A
+    need = L.hscale_output_error_workspace_bytes(T, n, m)
+    assert need > 0 and need % 8 == 0
+    assert L.hscale_output_error_workspace_bytes(0, n, m) == 0
+    assert L.hscale_output_error_workspace_bytes(T, 17, m) == 0
+    # the workspace is bounded: more than one pass of token tiles reuses it
+    assert L.hscale_output_error_workspace_bytes(10 ** 7, n, m) == L.hscale_output_error_workspace_bytes(2 ** 20, n, m)
+
+    def oe(**k):
+        return L.hscale_output_error(k.get("X", X), k.get("T", T), k.get("n", n), k.get("W", W), k.get("m", m),
+                                     k.get("s", 1e-3), k.get("codes", codes), k.get("packed", packed),
+                                     k.get("row", row), k.get("ws", ws), k.get("wsb", need), 0)
+    # every call fails validation: nothing is launched on the fake addresses
+    assert oe(n=17) == -2
+    assert oe(T=-1) == -2
+    assert oe(m=-3) == -2
+    assert oe(s=0.0) == -5
+    assert oe(X=0) == -1
+    assert oe(row=0) == -1
+    assert oe(ws=0) == -1
+    assert oe(X=X + 8) == -3
+    assert oe(W=W + 2) == -3
+    assert oe(packed=packed + 4) == -3
+    assert oe(row=row + 4) == -3
+    assert oe(ws=ws + 128) == -3
+    assert oe(wsb=need - 1) == -6
+    assert oe(row=X + 64) == -8         # output inside X
+    assert oe(ws=W) == -8               # workspace over W
+    assert oe(row=ws + 256) == -8       # output inside the workspace
+    # empty problems add nothing (no pointer needed)
+    assert L.hscale_output_error(0, 0, n, 0, m, 1e-3, 0, 0, 0, 0, 0, 0) == 0
+    assert L.hscale_output_error(0, T, n, 0, 0, 1e-3, 0, 0, 0, 0, 0, 0) == 0

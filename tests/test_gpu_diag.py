@@ -87,10 +87,12 @@ def test_search_stats_tiny(hs, tiny, init, down, up):
     r = rep["search"]["oracle"]
     so = oracle.shift_summary(r["shift"], r["e_best"], r["e_init"], down, up)
     # Groups whose shift differs from the oracle's are near-ties or 4over6
-    # anchor ties (compare_stats checked that); each moves one count.
+    # anchor ties (compare_stats checked that); each moves one count.  An
+    # anchor tie can also change the initial code (and so err_init) with the
+    # same shift; then its code differs too.
     differ = int((g["shift"] != r["shift"]).sum())
     assert np.abs(s["count"].astype(np.int64) - so["count"]).sum() <= 2 * differ
-    if differ == 0:
+    if differ == 0 and rep["search"]["tie_groups_differing"] == 0:
         for q in ("sum_init", "sum_best"):
             assert np.allclose(s[q], so[q], rtol=parity.ERR_REL_TOL, atol=0), q
         assert np.allclose(s["sum_rel"], so["sum_rel"], rtol=0, atol=4 * parity.ERR_REL_TOL * r["shift"].size)
@@ -142,3 +144,96 @@ def test_search_stats_full_size_sampled(hs):
           f"smaller={frac[:9].sum():.3f} removed={removed:.3f}", flush=True)
     assert rep["ok"], {k: v for k, v in rep.items() if k != "search"}
     assert 0.0 < removed < 1.0
+
+
+# ---------------------------------------------------------------------------
+# Layer-output error (Eq. 3)
+# ---------------------------------------------------------------------------
+
+# Tolerance of the per-row output error against the fp64 oracle.  dW enters
+# as hi + lo bf16 parts (relative error <= 2^-18 per element) and the
+# products are accumulated in fp32, so y_t = (X dW^T)_tr carries a sum of
+# independent rounding errors of about 2^-18 |x_tj dW_rj| each, which for
+# sign-mixed terms is of order 2^-18 |y_t|.  L_r = sum_t y_t^2 then has a
+# relative error of a few 1e-6, larger where a few tokens dominate the sum
+# (up to 1.3e-5 measured on the small cases); the bar leaves a margin of 8.
+LFULL_REL_TOL = 1e-4
+
+
+def _lfull_case(hs, T, n, m, seed, window=4, tokens_dev=None):
+    wl = CONFIGS["tiny"]
+    W = make_weight(wl, "cpu", shape=(m, n))
+    X = make_activations(wl, "cpu", tokens=T, n=n)
+    Wb, Xb = tensor_bits(W), tensor_bits(X)
+    s_g = harness_global_scale(W)
+    r = oracle.search(Wb, parity.oracle_h32(Xb), s_g, window=window)
+    return W, X, Wb, Xb, s_g, r["codes"], r["packed"]
+
+
+def _check_lfull(got, ref, label):
+    rel = np.abs(got - ref) / np.where(ref > 0, ref, 1.0)
+    print(f"[{label}] rows={len(ref)} max_rel={rel.max():.2e} total_rel="
+          f"{abs(got.sum() - ref.sum()) / ref.sum():.2e}", flush=True)
+    assert np.all(np.isfinite(got)) and rel.max() <= LFULL_REL_TOL, rel.max()
+
+
+@pytest.mark.parametrize("T,n,m", [(128, 512, 256), (300, 48, 130), (1, 16, 1), (257, 96, 129), (513, 1040, 77)])
+def test_output_error_matches_oracle(hs, T, n, m):
+    W, X, Wb, Xb, s_g, codes, packed = _lfull_case(hs, T, n, m, seed=T + n + m)
+    got = hs.output_error(X.to(DEV), W.to(DEV), s_g, torch.from_numpy(codes).to(DEV),
+                          torch.from_numpy(packed).to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle.output_error(Xb, oracle.delta(Wb, s_g, codes, packed))
+    _check_lfull(got.cpu().numpy(), ref, f"L_full {T}x{n}x{m}")
+
+
+def test_output_error_accumulates_and_code_zero(hs):
+    W, X, Wb, Xb, s_g, codes, packed = _lfull_case(hs, 700, 256, 200, seed=1)
+    codes = codes.copy()
+    codes[5, :] = 0  # zero scale: W^ = 0 on that row
+    Wd, Xd = W.to(DEV), X.to(DEV)
+    ct, pt = torch.from_numpy(codes).to(DEV), torch.from_numpy(packed).to(DEV)
+    whole = hs.output_error(Xd, Wd, s_g, ct, pt)
+    acc = torch.zeros(200, dtype=torch.float64, device=DEV)
+    for a, b in ((0, 1), (1, 256), (256, 700)):
+        hs.output_error(Xd[a:b].contiguous(), Wd, s_g, ct, pt, row_err=acc)
+    torch.cuda.synchronize()
+    ref = oracle.output_error(Xb, oracle.delta(Wb, s_g, codes, packed))
+    _check_lfull(whole.cpu().numpy(), ref, "L_full code 0")
+    _check_lfull(acc.cpu().numpy(), ref, "L_full 3 batches")
+    again = hs.output_error(Xd, Wd, s_g, ct, pt)
+    torch.cuda.synchronize()
+    assert torch.equal(again, whole)  # fixed-order sums: bitwise repeatable
+
+
+def test_output_error_two_passes(hs):
+    """More tokens than one tile launch covers (1024 tiles of 256): the
+    second pass adds its partials to the first."""
+    T, n, m = 262144 + 300, 64, 96
+    W, X, Wb, Xb, s_g, codes, packed = _lfull_case(hs, T, n, m, seed=2)
+    got = hs.output_error(X.to(DEV), W.to(DEV), s_g, torch.from_numpy(codes).to(DEV),
+                          torch.from_numpy(packed).to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle.output_error(Xb, oracle.delta(Wb, s_g, codes, packed))
+    _check_lfull(got.cpu().numpy(), ref, "L_full two passes")
+
+
+def test_output_error_full_size_sampled(hs):
+    """down_proj's full W (4096 x 14336) with 16384 calibration tokens, in the
+    launch configuration the benchmark uses; the stored tensor is made by the
+    oracle (max-abs codes shifted by seeded steps in -9..+6, quantized), and
+    sampled rows are checked against the oracle."""
+    wl = CONFIGS["down_proj"]
+    X = make_activations(wl, "cpu", tokens=16384)
+    Xb = tensor_bits(X)
+    W = make_weight(wl, DEV)
+    s_g = harness_global_scale(W)
+    Wb_all = tensor_bits(W)
+    c0 = oracle.anchor_codes(Wb_all, s_g, 6.0).astype(np.int64)
+    codes = np.clip(c0 + np.random.default_rng(5).integers(-9, 7, c0.shape), 1, 126).astype(np.uint8)
+    packed, _ = oracle.quantize(Wb_all, s_g, codes)
+    got = hs.output_error(X.to(DEV), W, s_g, torch.from_numpy(codes).to(DEV), torch.from_numpy(packed).to(DEV))
+    torch.cuda.synchronize()
+    rows = np.unique(np.r_[np.random.default_rng(4).choice(wl.out, 10, replace=False), 0, wl.out - 1])
+    ref = oracle.output_error(Xb, oracle.delta(Wb_all[rows], s_g, codes[rows], packed[rows]))
+    _check_lfull(got.cpu().numpy()[rows], ref, "L_full down_proj sampled")
