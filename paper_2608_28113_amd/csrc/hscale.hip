@@ -690,10 +690,23 @@ __global__ __launch_bounds__(64) void shift_summary_final(const double *__restri
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kLfBM = 256;  // tokens per tile
-constexpr int kLfBN = 128;  // weight rows per tile
-constexpr int kLfBK = 32;   // k per LDS stage (two 16-deep MFMA steps)
-constexpr int kLfThreads = 256;
+// Tile of X dW^T per block: kLfBM tokens x kLfBN weight rows, computed by
+// kLfWM x kLfWN waves (each a (kLfBM / kLfWM) x (kLfBN / kLfWN) sub-tile of
+// 32 x 32 MFMA accumulators).
+constexpr int kLfBM = 256;
+constexpr int kLfBN = 256;
+constexpr int kLfWM = 2;
+constexpr int kLfWN = 4;
+constexpr int kLfBK = 32;  // k per LDS stage (two 16-deep MFMA steps)
+constexpr int kLfThreads = 64 * kLfWM * kLfWN;
+constexpr int kLfMI = kLfBM / kLfWM / 32;  // accumulator tiles per wave, token direction
+constexpr int kLfNJ = kLfBN / kLfWN / 32;  // accumulator tiles per wave, weight-row direction
+constexpr int kLfRows = kLfBM + 2 * kLfBN;  // LDS rows of 64 bytes per stage (X, dW hi, dW lo)
+constexpr int kLfStages = 3;                // LDS ring depth: two stages in flight while one is used
+constexpr int kLfWaves = kLfThreads / 64;
+constexpr int kLfDmaPerWave = kLfRows / 16 / kLfWaves;  // 1 KB direct-to-LDS loads per wave per stage
+static_assert(kLfRows % (16 * kLfWaves) == 0 && kLfBM % 16 == 0 && kLfBN % 16 == 0, "stage split");
+static_assert(kLfStages * kLfRows * 64 <= 160 * 1024, "LDS ring exceeds the CU's 160 KB");
 constexpr int64_t kLfMaxTilesPerPass = 1024;  // token tiles per tile launch (bounds the workspace)
 
 __device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
@@ -702,12 +715,14 @@ __device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
 }
 
 // dW of one 16-weight group, split into hi / lo bf16 planes of row stride
-// ldd; groups beyond (out, in) in the padded planes are written as zeros.
+// ldd; groups beyond (out, in) in the padded planes are written as zeros, and
+// so are the 256 bytes at `zero` (the source of out-of-range X chunks).
 __global__ __launch_bounds__(256) void delta_split_kernel(const u32x4 *__restrict__ W, int64_t out, int64_t in,
                                                           float s_g, const uint8_t *__restrict__ codes,
                                                           const uint2 *__restrict__ packed, int64_t rows_pad,
                                                           int64_t ldd, u32x4 *__restrict__ hi,
-                                                          u32x4 *__restrict__ lo) {
+                                                          u32x4 *__restrict__ lo, u32x4 *__restrict__ zero) {
+    if (blockIdx.x == 0 && threadIdx.x < 16) zero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
     const int64_t Gp = ldd / kGroup, Gc = in / kGroup;
     const int64_t total = rows_pad * Gp;
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -752,11 +767,17 @@ __global__ __launch_bounds__(256) void delta_split_kernel(const u32x4 *__restric
 }
 
 // LDS tiles hold rows of kLfBK bf16 (64 bytes = four 16-byte chunks); chunk c
-// of row r lives at chunk position c ^ ((r >> 1) & 3) so that the 32 rows an
-// MFMA operand read touches spread over the banks.
+// of row r lives at chunk position c ^ ((r >> 2) & 3).  A 16-byte operand
+// read is served 16 lanes at a time over 64 four-byte banks (256 bytes); the
+// 16 consecutive rows those lanes read then fall in 16 distinct bank groups
+// (measured: no bank conflicts).
 __device__ __forceinline__ int lf_lds_offset(int row, int chunk) {
-    return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4);
+    return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
 }
+
+// s_waitcnt immediate (gfx9 encoding) waiting until at most n vector memory
+// operations of this wave are outstanding; the other counters are left free.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 struct LfArgs {
     const u32x4 *X;      // [tokens, in] bf16
@@ -764,105 +785,109 @@ struct LfArgs {
     const u32x4 *hi;     // [rows_pad, ldd] bf16 planes
     const u32x4 *lo;
     int64_t ldd;
-    int64_t out;           // weight rows
-    int64_t ntiles;        // rows_pad / kLfBN
-    double *partial;       // [token tiles of the pass, out]
+    int64_t out;      // weight rows
+    int64_t ntiles;   // rows_pad / kLfBN
+    double *partial;    // [token tiles of the pass, out]
+    const u32x4 *zero;  // 16 zero bytes, read for chunks outside X
 };
 
 __global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2][(kLfBM + 2 * kLfBN) * 64];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLfStages][kLfRows * 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % kLfWM, wn = wave / kLfWM;
     const int64_t mt = blockIdx.x / a.ntiles, nt = blockIdx.x % a.ntiles;
     const int64_t t0 = mt * kLfBM, r0 = nt * kLfBN;
     const int64_t xrow_vec = a.in / 8, drow_vec = a.ldd / 8;
-    const int stages = (int)((a.ldd) / kLfBK);
+    const int stages = (int)(a.ldd / kLfBK);
 
-    // Global -> register staging: 4 A chunks and 2 + 2 B chunks per thread.
-    u32x4 sa[4], sh[2], sl[2];
-    auto load_stage = [&](int s) {
+    // A stage is filled straight from global memory into LDS: each wave
+    // issues kLfDmaPerWave 16-byte-per-lane loads, each landing in 1 KB
+    // (16 rows) of the stage, lane l at row 16 kb + l / 4, position l % 4;
+    // the lane fetches the chunk that the swizzle stores at that position.
+    // Rows below kLfBM are X (out-of-range chunks read zeros), then dW hi,
+    // dW lo (padded planes, always in range).
+    auto issue = [&](int s, int buf) {
         const int64_t kvec = (int64_t)s * (kLfBK / 8);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
-            const int64_t t = t0 + row, kv = kvec + c;
-            sa[i] = (t < a.tokens && kv < xrow_vec) ? __builtin_nontemporal_load(a.X + t * xrow_vec + kv)
-                                                    : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
-            const int64_t off = (r0 + row) * drow_vec + kvec + c;
-            sh[i] = a.hi[off];
-            sl[i] = a.lo[off];
-        }
-    };
-    auto store_stage = [&](int buf) {
-        uint8_t *base = lds[buf];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
-            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(row, c)) = sa[i];
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int q = tid + i * kLfThreads, row = q >> 2, c = q & 3;
-            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(kLfBM + row, c)) = sh[i];
-            *reinterpret_cast<u32x4 *>(base + lf_lds_offset(kLfBM + kLfBN + row, c)) = sl[i];
+        for (int i = 0; i < kLfDmaPerWave; ++i) {
+            const int kb = wave + i * kLfWaves;
+            const int row = kb * 16 + (lane >> 2);
+            const int c = (lane & 3) ^ ((row >> 2) & 3);
+            const u32x4 *src;
+            if (kb < kLfBM / 16) {
+                const int64_t t = t0 + row, kv = kvec + c;
+                src = (t < a.tokens && kv < xrow_vec) ? a.X + t * xrow_vec + kv : a.zero;
+            } else {
+                const int rb = row - kLfBM;
+                const u32x4 *plane = rb < kLfBN ? a.hi : a.lo;
+                src = plane + (r0 + rb % kLfBN) * drow_vec + kvec + c;
+            }
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src),
+                                             (__attribute__((address_space(3))) void *)(lds[buf] + kb * 1024), 16,
+                                             0, 0);
         }
     };
 
-    f32x16 acc[4][2];
+    f32x16 acc[kLfMI][kLfNJ];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kLfMI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < kLfNJ; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
+    // Ring of kLfStages buffers: stage s + 2 is issued once every wave has
+    // finished reading stage s - 1 (the barrier), into that stage's buffer.
+    // Each wave first waits for its own loads of stage s (vmcnt counts them in
+    // issue order; the kLfDmaPerWave loads of stage s + 1 may stay in
+    // flight); the barrier then makes all of stage s visible.  A plain
+    // s_barrier is used: __syncthreads() adds a release fence that waits for
+    // every outstanding load, stage s + 1's included.
+    issue(0, 0);
+    if (stages > 1) issue(1, 1);
     for (int s = 0; s < stages; ++s) {
-        const bool more = s + 1 < stages;
-        if (more) load_stage(s + 1);
-        const uint8_t *base = lds[s & 1];
+        if (s + 1 < stages)
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLfDmaPerWave));
+        else
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        asm volatile("s_barrier" ::: "memory");
+        if (s + 2 < stages) issue(s + 2, (s + 2) % kLfStages);
+        const uint8_t *base = lds[s % kLfStages];
 #pragma unroll
         for (int kk = 0; kk < kLfBK / 16; ++kk) {
             const int c = 2 * kk + (lane >> 5);
-            bf16x8 fa[4], fh[2], fl[2];
+            bf16x8 fa[kLfMI], fh[kLfNJ], fl[kLfNJ];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = wm * 128 + i * 32 + (lane & 31);
+            for (int i = 0; i < kLfMI; ++i) {
+                const int row = wm * (kLfBM / kLfWM) + i * 32 + (lane & 31);
                 fa[i] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(row, c));
             }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int row = wn * 64 + j * 32 + (lane & 31);
+            for (int j = 0; j < kLfNJ; ++j) {
+                const int row = wn * (kLfBN / kLfWN) + j * 32 + (lane & 31);
                 fh[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + row, c));
                 fl[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + kLfBN + row, c));
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < kLfMI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
+                for (int j = 0; j < kLfNJ; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fh[j], acc[i][j], 0, 0, 0);
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fl[j], acc[i][j], 0, 0, 0);
                 }
         }
-        if (more) store_stage((s + 1) & 1);
-        __syncthreads();
     }
+    __syncthreads();
 
     // Column sums of squares: lane l holds column l % 32 of each 32x32
-    // accumulator; lanes l and l + 32 share a column, and waves wm = 0, 1
-    // share the wave's 64 columns.
-    double sq[2];
+    // accumulator; lanes l and l + 32 share a column, and the kLfWM waves of
+    // a column group share its columns (added in wm order).
+    double sq[kLfNJ];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < kLfNJ; ++j) {
         double v = 0.0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kLfMI; ++i)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const double y = (double)acc[i][j][e];
@@ -870,15 +895,18 @@ __global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) 
             }
         sq[j] = v + __shfl_xor(v, 32, 64);
     }
-    double *red = reinterpret_cast<double *>(lds[0]);  // [2 wm][128 columns]
+    double *red = reinterpret_cast<double *>(lds[0]);  // [kLfWM][kLfBN]
     if (lane < 32) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) red[wm * kLfBN + wn * 64 + j * 32 + lane] = sq[j];
+        for (int j = 0; j < kLfNJ; ++j) red[wm * kLfBN + wn * (kLfBN / kLfWN) + j * 32 + lane] = sq[j];
     }
     __syncthreads();
     if (tid < kLfBN) {
         const int64_t col = r0 + tid;
-        if (col < a.out) a.partial[mt * a.out + col] = red[tid] + red[kLfBN + tid];
+        double v = red[tid];
+#pragma unroll
+        for (int w = 1; w < kLfWM; ++w) v += red[w * kLfBN + tid];
+        if (col < a.out) a.partial[mt * a.out + col] = v;
     }
 }
 
@@ -1014,7 +1042,7 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
 
 struct LfPlan {
     int64_t ldd = 0, rows_pad = 0, ntiles = 0, tiles_per_pass = 0;
-    size_t plane_bytes = 0, partial_offset = 0, bytes = 0;
+    size_t plane_bytes = 0, zero_offset = 0, partial_offset = 0, bytes = 0;
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -1028,7 +1056,8 @@ LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
     const int64_t tiles = (tokens + kLfBM - 1) / kLfBM;
     p.tiles_per_pass = tiles < kLfMaxTilesPerPass ? tiles : kLfMaxTilesPerPass;
     p.plane_bytes = round_up((size_t)p.rows_pad * (size_t)p.ldd * 2, 256);
-    p.partial_offset = 2 * p.plane_bytes;
+    p.zero_offset = 2 * p.plane_bytes;
+    p.partial_offset = p.zero_offset + 256;
     p.bytes = p.partial_offset + (size_t)p.tiles_per_pass * (size_t)out * sizeof(double);
     return p;
 }
@@ -1245,7 +1274,8 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
     double *partial = reinterpret_cast<double *>(ws + p.partial_offset);
     hipLaunchKernelGGL(delta_split_kernel, dim3(grid_for(p.rows_pad * (p.ldd / kGroup))), dim3(256), 0, stream,
                        static_cast<const u32x4 *>(W), out, in, global_scale, scale_codes,
-                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo);
+                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo,
+                       reinterpret_cast<u32x4 *>(ws + p.zero_offset));
     if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
     const int64_t pass_tokens = p.tiles_per_pass * kLfBM;
     const unsigned tree_blocks = (unsigned)((out + kTreeCols - 1) / kTreeCols);
@@ -1260,6 +1290,7 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
         a.out = out;
         a.ntiles = p.ntiles;
         a.partial = partial;
+        a.zero = reinterpret_cast<const u32x4 *>(ws + p.zero_offset);
         const int64_t tiles = (a.tokens + kLfBM - 1) / kLfBM;
         hipLaunchKernelGGL(lfull_tile_kernel, dim3((unsigned)(tiles * p.ntiles)), dim3(kLfThreads), 0, stream, a);
         if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
