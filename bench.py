@@ -38,6 +38,7 @@ import numpy as np
 
 METRIC = "H-Scale search Gweights/s + hdiag HBM GB/s (fraction of peak), 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 # fp32 VALU issue ceiling: 256 CU x 4 SIMD x 32 lanes/clk (one wave64 fp32
 # op per 2 clocks) x 2.4 GHz = 78.64 T lane-ops/s = 157.3 TFLOP/s of FMA.
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
@@ -97,6 +98,10 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=32768,
                     help="tokens of X in the CPU oracle hdiag sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-diagnostics", action="store_true",
+                    help="skip the quality-diagnostics leg (shift statistics, Eq. 3 output error)")
+    ap.add_argument("--diag-profile", action="store_true",
+                    help="run only the diagnostics kernels on the workload's last layer (for rocprofv3)")
     ap.add_argument("--profile-mode", action="store_true",
                     help="only warm-up and timed steps (for rocprofv3 runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -155,6 +160,12 @@ def main():
     acts, layers, desc = build_workload(args.workload, dev, args.window)
     if args.down is not None:
         layers = [(l, W, xk, s, None) for (l, W, xk, s, _) in layers]
+    if args.diag_profile:
+        diag = diag_leg(args, acts, layers, repeats=2)
+        if args.copy_calibration:
+            copy_calibration(dev)
+        print(json.dumps({"diag_profile": True, "diagnostics": diag}), flush=True)
+        return
     hbuf = {k: torch.empty(X.shape[1], dtype=torch.float32, device=dev) for k, X in acts.items()}
     ws = torch.empty(max(max(hs.hdiag_workspace_bytes(*X.shape) for X in acts.values()), 16),
                      dtype=torch.uint8, device=dev)
@@ -200,13 +211,7 @@ def main():
     t_s = np.array([e[nh].elapsed_time(e[-1]) for e in events]) * 1e-3  # all search calls of a step
     t_step = np.array([e[0].elapsed_time(e[-1]) for e in events]) * 1e-3
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        src.fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(dev)
     if args.profile_mode:
         print(json.dumps({"profile_mode": True, "hdiag_ms": float(t_h.mean() * 1e3),
                           "search_ms": float(t_s.mean() * 1e3)}), flush=True)
@@ -271,7 +276,90 @@ def main():
     }
     if not args.no_cpu_baseline:
         out.update(cpu_leg(args, acts, layers))
+    if not args.no_diagnostics:
+        out["diagnostics"] = diag_leg(args, acts, layers)
     print(json.dumps(out), flush=True)
+
+
+def copy_calibration(dev):
+    """One plain 1 GiB device-to-device copy: a kernel of known traffic for
+    scaling the HBM byte counters."""
+    import torch
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def diag_leg(args, acts, layers, repeats=5):
+    """Quality diagnostics of the paper's appendix on the workload's last
+    layer, outside the timed hot-path steps: the search with per-group
+    statistics and their per-shift summary (selected-shift figure), and the
+    Eq. 3 layer-output error L_full of the max-abs codes and of the searched
+    codes (window-sweep metric).  The output-error kernel is timed with HIP
+    events on the stream it runs on and priced against the bf16 matrix-core
+    peak with its algorithmic 2 T n m flops (it issues twice that: the
+    rounding error enters as two bf16 parts)."""
+    import torch
+    import paper_2608_28113_amd as hs
+
+    lname, W, xk, s_g, w = layers[-1]
+    X = acts[xk]
+    down, up = (w, w) if w is not None else (args.down, args.up)
+    stream = torch.cuda.current_stream()
+    T, n = X.shape
+    m = W.shape[0]
+    h = hs.hdiag(X)
+
+    def timed(fn):
+        ts, res = [], None
+        for _ in range(repeats):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            res = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return res, float(np.median(ts))
+
+    st, t_stats = timed(lambda: hs.search_stats(W, h, s_g, down, up, init=args.init, stream=stream))
+    summ, t_summ = timed(lambda: hs.shift_summary(st["shift"], st["err_best"], st["err_init"], down, up,
+                                                   stream=stream))
+    count = summ["count"].cpu().numpy().astype(np.float64)
+    si, sb = summ["sum_init"].cpu().numpy(), summ["sum_best"].cpu().numpy()
+    frac = count / count.sum()
+    ws = torch.empty(max(hs.output_error_workspace_bytes(T, n, m), 256), dtype=torch.uint8, device=X.device)
+    row = torch.zeros(m, dtype=torch.float64, device=X.device)
+
+    def lfull(codes, packed):
+        row.zero_()
+        hs.output_error(X, W, s_g, codes, packed, row_err=row, workspace=ws, stream=stream)
+        return row
+
+    L_search, t_lf = timed(lambda: lfull(st["scale_codes"], st["packed_e2m1"]))
+    L_search = float(L_search.sum().item())
+    c0, p0 = hs.search(W, h, s_g, window=0, init=args.init, stream=stream)
+    L_init = float(lfull(c0, p0).sum().item())
+    flops = 2.0 * T * n * m
+    tf = flops / (t_lf * 1e-3) / 1e12
+    return {
+        "layer": lname, "window": [down, up], "init": args.init, "tokens": T,
+        "shift_fractions": {"keep": round(float(frac[down]), 4), "larger": round(float(frac[down + 1:].sum()), 4),
+                            "smaller": round(float(frac[:down].sum()), 4)},
+        "shift_histogram": {str(d): int(c) for d, c in zip(range(-down, up + 1), count)},
+        "surrogate_error_removed": round(float(1.0 - sb.sum() / si.sum()), 4),
+        "L_full_init": L_init, "L_full_search": L_search,
+        "L_full_reduction": round(1.0 - L_search / L_init, 4),
+        "search_stats_ms": round(t_stats, 4), "shift_summary_ms": round(t_summ, 4),
+        "output_error_ms": round(t_lf, 3),
+        "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "hscale_output_error (delta_split_kernel + lfull_tile_kernel + hdiag_tree)",
+                     "algorithmic_flops": flops, "issued_mfma_flops": 2 * flops},
+    }
 
 
 def cpu_leg(args, acts, layers):
