@@ -44,7 +44,17 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
 SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
 HERE = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SRC = os.path.join(HERE, "paper_2608_28113_amd", "csrc", "hscale.hip")
+# Sources of the hot-path kernels (hdiag, search): the committed HBM-traffic
+# figures are valid only for the source they were measured on.
+HOT_SOURCES = [os.path.join(HERE, "paper_2608_28113_amd", "csrc", f) for f in ("common.h", "hdiag.hip", "search.hip")]
+
+
+def hot_source_hash() -> str:
+    h = hashlib.sha256()
+    for path in HOT_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def search_ops_per_weight(K: int, init: str) -> int:
@@ -68,9 +78,7 @@ def measured_traffic(workload: str):
         return None
     with open(path) as f:
         prof = json.load(f)
-    with open(KERNEL_SRC, "rb") as f:
-        src = hashlib.sha256(f.read()).hexdigest()[:16]
-    if prof.get("kernel_source_sha256_16") != src:
+    if prof.get("kernel_source_sha256_16") != hot_source_hash():
         return None
     t = prof.get("traffic", {})
 

@@ -13,7 +13,8 @@ from pathlib import Path
 
 PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
-SRC = PKG / "csrc" / "hscale.hip"
+CSRC = PKG / "csrc"
+SOURCES = [CSRC / "hdiag.hip", CSRC / "search.hip", CSRC / "diag.hip"]  # share csrc/common.h
 INCLUDE = ROOT / "include"
 LIB = PKG / "libhscale.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -28,7 +29,7 @@ FLAGS = [
 
 def build(verbose: bool = False) -> Path:
     tmp = LIB.with_suffix(".so.tmp%d" % os.getpid())
-    cmd = [HIPCC, *FLAGS, "-I", str(INCLUDE), "-o", str(tmp), str(SRC)]
+    cmd = [HIPCC, *FLAGS, "-I", str(INCLUDE), "-I", str(CSRC), "-o", str(tmp), *map(str, SOURCES)]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

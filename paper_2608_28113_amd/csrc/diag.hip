@@ -1,0 +1,531 @@
+// Quality diagnostics of the paper's appendix behind the C ABI of
+// include/hscale.h: the per-shift summary of the search statistics and the
+// layer-output error of Eq. 3.
+
+#include "common.h"
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Selected-shift statistics (the paper's appendix on selected scale shifts):
+// per shift d, the number of groups that chose it and the fp64 sums of their
+// initial errors, chosen errors and relative reductions.  Deterministic: each
+// block reduces a fixed chunk in a fixed order, then one wave per bin sums
+// the block partials in a fixed order.
+// ---------------------------------------------------------------------------
+
+constexpr int kSumThreads = 256;
+constexpr int kSumPerThread = 16;
+constexpr int kSumChunk = kSumThreads * kSumPerThread;
+constexpr int kSumOutside = 1 << 20;  // shift value standing for "no group"
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// Block b reduces groups [b * kSumChunk, (b + 1) * kSumChunk) into
+// part[(b * K + k) * 3 + {0: init, 1: best, 2: rel}] and cnt[b * K + k] for
+// every bin k = d + down (zeros for bins no group of the chunk chose).
+__global__ __launch_bounds__(kSumThreads) void shift_summary_partial(const int8_t *__restrict__ shift,
+                                                                     const float *__restrict__ err_best,
+                                                                     const float *__restrict__ err_init,
+                                                                     int64_t groups, int down, int up,
+                                                                     double *__restrict__ part,
+                                                                     uint32_t *__restrict__ cnt) {
+    __shared__ double red[kSumThreads / 64][3];
+    __shared__ uint32_t redc[kSumThreads / 64];
+    __shared__ int lim[2][kSumThreads / 64];
+    const int K = down + up + 1;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t base = (int64_t)blockIdx.x * kSumChunk;
+    int d[kSumPerThread];
+    float eb[kSumPerThread], ei[kSumPerThread];
+    int lo = kSumOutside, hi = -kSumOutside;
+#pragma unroll
+    for (int e = 0; e < kSumPerThread; ++e) {
+        const int64_t g = base + threadIdx.x + (int64_t)e * kSumThreads;
+        d[e] = kSumOutside;
+        eb[e] = ei[e] = 0.0f;
+        if (g < groups) {
+            const int v = shift[g];
+            if (v >= -down && v <= up) {
+                d[e] = v;
+                eb[e] = err_best[g];
+                ei[e] = err_init[g];
+                lo = min(lo, v);
+                hi = max(hi, v);
+            }
+        }
+    }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    if (lane == 0) {
+        lim[0][wave] = lo;
+        lim[1][wave] = hi;
+    }
+    __syncthreads();
+    lo = min(min(lim[0][0], lim[0][1]), min(lim[0][2], lim[0][3]));
+    hi = max(max(lim[1][0], lim[1][1]), max(lim[1][2], lim[1][3]));
+    double *bp = part + (size_t)blockIdx.x * K * 3;
+    uint32_t *bc = cnt + (size_t)blockIdx.x * K;
+    for (int k = threadIdx.x; k < K; k += kSumThreads) {
+        if (k - down < lo || k - down > hi) {
+            bp[3 * k] = bp[3 * k + 1] = bp[3 * k + 2] = 0.0;
+            bc[k] = 0u;
+        }
+    }
+    for (int v = lo; v <= hi; ++v) {  // block-uniform bounds
+        double si = 0.0, sb = 0.0, sr = 0.0;
+        uint32_t c = 0;
+#pragma unroll
+        for (int e = 0; e < kSumPerThread; ++e) {
+            if (d[e] == v) {
+                const double a = ei[e], b = eb[e];
+                ++c;
+                si += a;
+                sb += b;
+                sr += a > 0.0 ? (a - b) / a : 0.0;
+            }
+        }
+        si = wave_sum(si);
+        sb = wave_sum(sb);
+        sr = wave_sum(sr);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+        if (lane == 0) {
+            red[wave][0] = si;
+            red[wave][1] = sb;
+            red[wave][2] = sr;
+            redc[wave] = c;
+        }
+        __syncthreads();
+        if (threadIdx.x < 3) {
+            const int q = threadIdx.x;
+            bp[3 * (v + down) + q] = (red[0][q] + red[1][q]) + (red[2][q] + red[3][q]);
+        } else if (threadIdx.x == 3) {
+            bc[v + down] = (redc[0] + redc[1]) + (redc[2] + redc[3]);
+        }
+        __syncthreads();
+    }
+}
+
+// One wave per bin: lane l sums the partials of blocks l, l + 64, ... in
+// order, then a fixed butterfly combines the lanes.
+__global__ __launch_bounds__(64) void shift_summary_final(const double *__restrict__ part,
+                                                          const uint32_t *__restrict__ cnt, int64_t blocks,
+                                                          int K, uint64_t *__restrict__ count,
+                                                          double *__restrict__ sum_init,
+                                                          double *__restrict__ sum_best,
+                                                          double *__restrict__ sum_rel) {
+    const int k = blockIdx.x;
+    double si = 0.0, sb = 0.0, sr = 0.0;
+    uint64_t c = 0;
+    for (int64_t b = threadIdx.x; b < blocks; b += 64) {
+        const double *p = part + ((size_t)b * K + k) * 3;
+        si += p[0];
+        sb += p[1];
+        sr += p[2];
+        c += cnt[(size_t)b * K + k];
+    }
+    si = wave_sum(si);
+    sb = wave_sum(sb);
+    sr = wave_sum(sr);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (threadIdx.x == 0) {
+        count[k] = c;
+        sum_init[k] = si;
+        sum_best[k] = sb;
+        sum_rel[k] = sr;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Layer-output error (Sec. 3.2, Eq. 3): L_r = sum_t (X dW^T)_tr^2 per output
+// row r, with dW = W - W^ the rounding error of a stored NVFP4 tensor.
+//
+// dW is formed once in fp32 (w - v S[c], one rounding) and split into two
+// bf16 planes hi + lo (|dW - hi - lo| <= 2^-18 |dW|), so X dW^T is two bf16
+// MFMA products accumulated in fp32.  Each block computes a 256-token x
+// 128-row tile of X dW^T in registers and reduces the squares of its columns
+// in fp64; the tile is never written.  Per-tile column sums go to a
+// workspace and a fixed-order tree adds them to row_err.
+// ---------------------------------------------------------------------------
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Tile of X dW^T per block: kLfBM tokens x kLfBN weight rows, computed by
+// kLfWM x kLfWN waves (each a (kLfBM / kLfWM) x (kLfBN / kLfWN) sub-tile of
+// 32 x 32 MFMA accumulators).
+constexpr int kLfBM = 256;
+constexpr int kLfBN = 256;
+constexpr int kLfWM = 2;
+constexpr int kLfWN = 4;
+constexpr int kLfBK = 32;  // k per LDS stage (two 16-deep MFMA steps)
+constexpr int kLfThreads = 64 * kLfWM * kLfWN;
+constexpr int kLfMI = kLfBM / kLfWM / 32;  // accumulator tiles per wave, token direction
+constexpr int kLfNJ = kLfBN / kLfWN / 32;  // accumulator tiles per wave, weight-row direction
+constexpr int kLfRows = kLfBM + 2 * kLfBN;  // LDS rows of 64 bytes per stage (X, dW hi, dW lo)
+constexpr int kLfStages = 3;                // LDS ring depth: two stages in flight while one is used
+constexpr int kLfWaves = kLfThreads / 64;
+constexpr int kLfDmaPerWave = kLfRows / 16 / kLfWaves;  // 1 KB direct-to-LDS loads per wave per stage
+static_assert(kLfRows % (16 * kLfWaves) == 0 && kLfBM % 16 == 0 && kLfBN % 16 == 0, "stage split");
+static_assert(kLfStages * kLfRows * 64 <= 160 * 1024, "LDS ring exceeds the CU's 160 KB");
+constexpr int64_t kLfMaxTilesPerPass = 1024;  // token tiles per tile launch (bounds the workspace)
+
+__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;  // finite inputs
+}
+
+// dW of one 16-weight group, split into hi / lo bf16 planes of row stride
+// ldd; groups beyond (out, in) in the padded planes are written as zeros, and
+// so are the 256 bytes at `zero` (the source of out-of-range X chunks).
+__global__ __launch_bounds__(256) void delta_split_kernel(const u32x4 *__restrict__ W, int64_t out, int64_t in,
+                                                          float s_g, const uint8_t *__restrict__ codes,
+                                                          const uint2 *__restrict__ packed, int64_t rows_pad,
+                                                          int64_t ldd, u32x4 *__restrict__ hi,
+                                                          u32x4 *__restrict__ lo, u32x4 *__restrict__ zero) {
+    if (blockIdx.x == 0 && threadIdx.x < 16) zero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+    const int64_t Gp = ldd / kGroup, Gc = in / kGroup;
+    const int64_t total = rows_pad * Gp;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total; q += stride) {
+        const int64_t r = q / Gp, i = q % Gp;
+        uint32_t hb[8], lb[8];
+        if (r < out && i < Gc) {
+            const int64_t g = r * Gc + i;
+            float w[kGroup];
+            load_group(W, g, w);
+            const float S = s_g * e4m3fn_value(codes[g]);
+            const uint2 p = packed[g];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const uint32_t src = k < 4 ? p.x : p.y;
+                float2 v;
+                switch (k & 3) {
+                    case 0: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 0); v = make_float2(t[0], t[1]); break; }
+                    case 1: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 1); v = make_float2(t[0], t[1]); break; }
+                    case 2: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 2); v = make_float2(t[0], t[1]); break; }
+                    default: { const auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, 3); v = make_float2(t[0], t[1]); break; }
+                }
+                const float d0 = fmaf(-v.x, S, w[2 * k]);
+                const float d1 = fmaf(-v.y, S, w[2 * k + 1]);
+                const uint32_t h0 = bf16_bits_rne(d0), h1 = bf16_bits_rne(d1);
+                const uint32_t l0 = bf16_bits_rne(d0 - __uint_as_float(h0 << 16));
+                const uint32_t l1 = bf16_bits_rne(d1 - __uint_as_float(h1 << 16));
+                hb[k] = h0 | (h1 << 16);
+                lb[k] = l0 | (l1 << 16);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) hb[k] = lb[k] = 0u;
+        }
+        u32x4 *dh = hi + (r * ldd + i * kGroup) / 8;
+        u32x4 *dl = lo + (r * ldd + i * kGroup) / 8;
+        dh[0] = u32x4{hb[0], hb[1], hb[2], hb[3]};
+        dh[1] = u32x4{hb[4], hb[5], hb[6], hb[7]};
+        dl[0] = u32x4{lb[0], lb[1], lb[2], lb[3]};
+        dl[1] = u32x4{lb[4], lb[5], lb[6], lb[7]};
+    }
+}
+
+// LDS tiles hold rows of kLfBK bf16 (64 bytes = four 16-byte chunks); chunk c
+// of row r lives at chunk position c ^ ((r >> 2) & 3).  A 16-byte operand
+// read is served 16 lanes at a time over 64 four-byte banks (256 bytes); the
+// 16 consecutive rows those lanes read then fall in 16 distinct bank groups
+// (measured: no bank conflicts).
+__device__ __forceinline__ int lf_lds_offset(int row, int chunk) {
+    return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
+}
+
+// s_waitcnt immediate (gfx9 encoding) waiting until at most n vector memory
+// operations of this wave are outstanding; the other counters are left free.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+struct LfArgs {
+    const u32x4 *X;      // [tokens, in] bf16
+    int64_t tokens, in;  // of this pass
+    const u32x4 *hi;     // [rows_pad, ldd] bf16 planes
+    const u32x4 *lo;
+    int64_t ldd;
+    int64_t out;      // weight rows
+    int64_t ntiles;   // rows_pad / kLfBN
+    double *partial;    // [token tiles of the pass, out]
+    const u32x4 *zero;  // 16 zero bytes, read for chunks outside X
+};
+
+__global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLfStages][kLfRows * 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % kLfWM, wn = wave / kLfWM;
+    const int64_t mt = blockIdx.x / a.ntiles, nt = blockIdx.x % a.ntiles;
+    const int64_t t0 = mt * kLfBM, r0 = nt * kLfBN;
+    const int64_t xrow_vec = a.in / 8, drow_vec = a.ldd / 8;
+    const int stages = (int)(a.ldd / kLfBK);
+
+    // A stage is filled straight from global memory into LDS: each wave
+    // issues kLfDmaPerWave 16-byte-per-lane loads, each landing in 1 KB
+    // (16 rows) of the stage, lane l at row 16 kb + l / 4, position l % 4;
+    // the lane fetches the chunk that the swizzle stores at that position.
+    // Rows below kLfBM are X (out-of-range chunks read zeros), then dW hi,
+    // dW lo (padded planes, always in range).
+    auto issue = [&](int s, int buf) {
+        const int64_t kvec = (int64_t)s * (kLfBK / 8);
+#pragma unroll
+        for (int i = 0; i < kLfDmaPerWave; ++i) {
+            const int kb = wave + i * kLfWaves;
+            const int row = kb * 16 + (lane >> 2);
+            const int c = (lane & 3) ^ ((row >> 2) & 3);
+            const u32x4 *src;
+            if (kb < kLfBM / 16) {
+                const int64_t t = t0 + row, kv = kvec + c;
+                src = (t < a.tokens && kv < xrow_vec) ? a.X + t * xrow_vec + kv : a.zero;
+            } else {
+                const int rb = row - kLfBM;
+                const u32x4 *plane = rb < kLfBN ? a.hi : a.lo;
+                src = plane + (r0 + rb % kLfBN) * drow_vec + kvec + c;
+            }
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src),
+                                             (__attribute__((address_space(3))) void *)(lds[buf] + kb * 1024), 16,
+                                             0, 0);
+        }
+    };
+
+    f32x16 acc[kLfMI][kLfNJ];
+#pragma unroll
+    for (int i = 0; i < kLfMI; ++i)
+#pragma unroll
+        for (int j = 0; j < kLfNJ; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    // Ring of kLfStages buffers: stage s + 2 is issued once every wave has
+    // finished reading stage s - 1 (the barrier), into that stage's buffer.
+    // Each wave first waits for its own loads of stage s (vmcnt counts them in
+    // issue order; the kLfDmaPerWave loads of stage s + 1 may stay in
+    // flight); the barrier then makes all of stage s visible.  A plain
+    // s_barrier is used: __syncthreads() adds a release fence that waits for
+    // every outstanding load, stage s + 1's included.
+    issue(0, 0);
+    if (stages > 1) issue(1, 1);
+    for (int s = 0; s < stages; ++s) {
+        if (s + 1 < stages)
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLfDmaPerWave));
+        else
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        asm volatile("s_barrier" ::: "memory");
+        if (s + 2 < stages) issue(s + 2, (s + 2) % kLfStages);
+        const uint8_t *base = lds[s % kLfStages];
+#pragma unroll
+        for (int kk = 0; kk < kLfBK / 16; ++kk) {
+            const int c = 2 * kk + (lane >> 5);
+            bf16x8 fa[kLfMI], fh[kLfNJ], fl[kLfNJ];
+#pragma unroll
+            for (int i = 0; i < kLfMI; ++i) {
+                const int row = wm * (kLfBM / kLfWM) + i * 32 + (lane & 31);
+                fa[i] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(row, c));
+            }
+#pragma unroll
+            for (int j = 0; j < kLfNJ; ++j) {
+                const int row = wn * (kLfBN / kLfWN) + j * 32 + (lane & 31);
+                fh[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + row, c));
+                fl[j] = *reinterpret_cast<const bf16x8 *>(base + lf_lds_offset(kLfBM + kLfBN + row, c));
+            }
+#pragma unroll
+            for (int i = 0; i < kLfMI; ++i)
+#pragma unroll
+                for (int j = 0; j < kLfNJ; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fh[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fl[j], acc[i][j], 0, 0, 0);
+                }
+        }
+    }
+    __syncthreads();
+
+    // Column sums of squares: lane l holds column l % 32 of each 32x32
+    // accumulator; lanes l and l + 32 share a column, and the kLfWM waves of
+    // a column group share its columns (added in wm order).
+    double sq[kLfNJ];
+#pragma unroll
+    for (int j = 0; j < kLfNJ; ++j) {
+        double v = 0.0;
+#pragma unroll
+        for (int i = 0; i < kLfMI; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const double y = (double)acc[i][j][e];
+                v = fma(y, y, v);
+            }
+        sq[j] = v + __shfl_xor(v, 32, 64);
+    }
+    double *red = reinterpret_cast<double *>(lds[0]);  // [kLfWM][kLfBN]
+    if (lane < 32) {
+#pragma unroll
+        for (int j = 0; j < kLfNJ; ++j) red[wm * kLfBN + wn * (kLfBN / kLfWN) + j * 32 + lane] = sq[j];
+    }
+    __syncthreads();
+    if (tid < kLfBN) {
+        const int64_t col = r0 + tid;
+        double v = red[tid];
+#pragma unroll
+        for (int w = 1; w < kLfWM; ++w) v += red[w * kLfBN + tid];
+        if (col < a.out) a.partial[mt * a.out + col] = v;
+    }
+}
+
+struct LfPlan {
+    int64_t ldd = 0, rows_pad = 0, ntiles = 0, tiles_per_pass = 0;
+    size_t plane_bytes = 0, zero_offset = 0, partial_offset = 0, bytes = 0;
+};
+
+LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
+    LfPlan p;
+    if (tokens <= 0 || in <= 0 || out <= 0) return p;
+    p.ldd = (in + kLfBK - 1) / kLfBK * kLfBK;
+    p.rows_pad = (out + kLfBN - 1) / kLfBN * kLfBN;
+    p.ntiles = p.rows_pad / kLfBN;
+    const int64_t tiles = (tokens + kLfBM - 1) / kLfBM;
+    p.tiles_per_pass = tiles < kLfMaxTilesPerPass ? tiles : kLfMaxTilesPerPass;
+    p.plane_bytes = round_up((size_t)p.rows_pad * (size_t)p.ldd * 2, 256);
+    p.zero_offset = 2 * p.plane_bytes;
+    p.partial_offset = p.zero_offset + 256;
+    p.bytes = p.partial_offset + (size_t)p.tiles_per_pass * (size_t)out * sizeof(double);
+    return p;
+}
+
+int64_t summary_blocks(int64_t groups) { return groups > 0 ? (groups + kSumChunk - 1) / kSumChunk : 0; }
+
+}  // namespace
+
+extern "C" {
+
+size_t hscale_shift_summary_workspace_bytes(int64_t groups, int32_t down, int32_t up) {
+    if (groups <= 0 || down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow || groups > kMaxGroups) return 0;
+    const size_t K = (size_t)(down + up + 1);
+    return (size_t)summary_blocks(groups) * K * (3 * sizeof(double) + sizeof(uint32_t));
+}
+
+int hscale_shift_summary(const int8_t *shift, const float *err_best, const float *err_init, int64_t groups,
+                         int32_t down, int32_t up, uint64_t *count, double *sum_init, double *sum_best,
+                         double *sum_rel, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (groups < 0 || groups > kMaxGroups) return HSCALE_ERR_SHAPE;
+    if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
+    const int K = down + up + 1;
+    if (!count || !sum_init || !sum_best || !sum_rel) return HSCALE_ERR_NULL;
+    if (!aligned(count, 8) || !aligned(sum_init, 8) || !aligned(sum_best, 8) || !aligned(sum_rel, 8))
+        return HSCALE_ERR_ALIGN;
+    const size_t nk = (size_t)K * 8;
+    const void *outs[4] = {count, sum_init, sum_best, sum_rel};
+    for (int a = 0; a < 4; ++a)
+        for (int b = a + 1; b < 4; ++b)
+            if (overlaps(outs[a], nk, outs[b], nk)) return HSCALE_ERR_OVERLAP;
+    const int64_t blocks = summary_blocks(groups);
+    const size_t need = hscale_shift_summary_workspace_bytes(groups, down, up);
+    if (groups > 0) {
+        if (!shift || !err_best || !err_init) return HSCALE_ERR_NULL;
+        if (!aligned(err_best, 4) || !aligned(err_init, 4)) return HSCALE_ERR_ALIGN;
+        if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
+        if (!workspace) return HSCALE_ERR_NULL;
+        if (!aligned(workspace, 8)) return HSCALE_ERR_ALIGN;
+        const size_t g = (size_t)groups;
+        const struct {
+            const void *p;
+            size_t n;
+        } in_bufs[] = {{shift, g}, {err_best, g * 4}, {err_init, g * 4}, {workspace, need}};
+        for (int a = 0; a < 4; ++a)
+            for (const auto &b : in_bufs)
+                if (overlaps(outs[a], nk, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+        for (int a = 0; a < 3; ++a)
+            if (overlaps(workspace, need, in_bufs[a].p, in_bufs[a].n)) return HSCALE_ERR_OVERLAP;
+    }
+    double *part = static_cast<double *>(workspace);
+    uint32_t *cnt = blocks > 0 ? reinterpret_cast<uint32_t *>(part + (size_t)blocks * K * 3) : nullptr;
+    if (blocks > 0) {
+        hipLaunchKernelGGL(shift_summary_partial, dim3((unsigned)blocks), dim3(kSumThreads), 0, stream, shift,
+                           err_best, err_init, groups, down, up, part, cnt);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    }
+    hipLaunchKernelGGL(shift_summary_final, dim3((unsigned)K), dim3(64), 0, stream, part, cnt, blocks, K, count,
+                       sum_init, sum_best, sum_rel);
+    return launch_status();
+}
+
+size_t hscale_output_error_workspace_bytes(int64_t tokens, int64_t in, int64_t out) {
+    if (in % kGroup != 0 || in > ((int64_t)1 << 40) || (in > 0 && out > kMaxGroups / (in / kGroup))) return 0;
+    return lfull_plan(tokens, in, out).bytes;
+}
+
+int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W, int64_t out, float global_scale,
+                        const uint8_t *scale_codes, const uint8_t *packed_e2m1, double *row_err, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+    if (tokens < 0 || in < 0 || out < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    if (in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+    if (!scale_ok(global_scale)) return HSCALE_ERR_SCALE;
+    if (tokens == 0 || in == 0 || out == 0) return HSCALE_OK;  // adds nothing
+    if (!X || !W || !scale_codes || !packed_e2m1 || !row_err || !workspace) return HSCALE_ERR_NULL;
+    if (!aligned(X, 16) || !aligned(W, 16) || !aligned(packed_e2m1, 8) || !aligned(row_err, 8) ||
+        !aligned(workspace, 256))
+        return HSCALE_ERR_ALIGN;
+    const LfPlan p = lfull_plan(tokens, in, out);
+    if (workspace_bytes < p.bytes) return HSCALE_ERR_WORKSPACE;
+    const size_t nx = (size_t)tokens * (size_t)in * 2, nw = (size_t)out * (size_t)in * 2;
+    const size_t nc = (size_t)out * (size_t)(in / kGroup), np = (size_t)out * (size_t)(in / 2);
+    const size_t nr = (size_t)out * 8;
+    const struct {
+        const void *p;
+        size_t n;
+    } ins[] = {{X, nx}, {W, nw}, {scale_codes, nc}, {packed_e2m1, np}};
+    for (const auto &b : ins)
+        if (overlaps(row_err, nr, b.p, b.n) || overlaps(workspace, p.bytes, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+    if (overlaps(row_err, nr, workspace, p.bytes)) return HSCALE_ERR_OVERLAP;
+
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    u32x4 *hi = reinterpret_cast<u32x4 *>(ws), *lo = reinterpret_cast<u32x4 *>(ws + p.plane_bytes);
+    double *partial = reinterpret_cast<double *>(ws + p.partial_offset);
+    hipLaunchKernelGGL(delta_split_kernel, dim3(grid_for(p.rows_pad * (p.ldd / kGroup), 256)), dim3(256), 0, stream,
+                       static_cast<const u32x4 *>(W), out, in, global_scale, scale_codes,
+                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo,
+                       reinterpret_cast<u32x4 *>(ws + p.zero_offset));
+    if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    const int64_t pass_tokens = p.tiles_per_pass * kLfBM;
+    const unsigned tree_blocks = (unsigned)((out + kTreeCols - 1) / kTreeCols);
+    for (int64_t t0 = 0; t0 < tokens; t0 += pass_tokens) {
+        LfArgs a;
+        a.tokens = tokens - t0 < pass_tokens ? tokens - t0 : pass_tokens;
+        a.in = in;
+        a.X = static_cast<const u32x4 *>(X) + t0 * (in / 8);
+        a.hi = hi;
+        a.lo = lo;
+        a.ldd = p.ldd;
+        a.out = out;
+        a.ntiles = p.ntiles;
+        a.partial = partial;
+        a.zero = reinterpret_cast<const u32x4 *>(ws + p.zero_offset);
+        const int64_t tiles = (a.tokens + kLfBM - 1) / kLfBM;
+        hipLaunchKernelGGL(lfull_tile_kernel, dim3((unsigned)(tiles * p.ntiles)), dim3(kLfThreads), 0, stream, a);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+        hipLaunchKernelGGL(hdiag_tree<true>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
+                           static_cast<const double *>(partial), tiles, out, (float *)nullptr, row_err);
+        if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
+    }
+    return HSCALE_OK;
+}
+
+}  // extern "C"

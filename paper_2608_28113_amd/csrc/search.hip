@@ -1,0 +1,431 @@
+// The per-group NVFP4 scale search (Sec. 3.3, Eq. 7, 9-13) and the final
+// re-quantization, behind the C ABI of include/hscale.h.
+//
+//   search  one 16-weight group per lane, lanes over consecutive groups (a
+//           wave reads 2 KiB of W contiguously and writes 512 contiguous
+//           bytes of codes).  The 126-entry table of (S[c], R[c]) lives in
+//           LDS.  Per candidate: 16 fp32 products w R, 8 hardware E2M1
+//           down-conversions (packed nibbles with sign, round-to-nearest-
+//           even, saturating at 6), 8 up-conversions back to grid values, 16
+//           residual FMAs w - v S (one rounding each) and a 4x4 fp32
+//           accumulation of h r^2.  The best candidate's packed nibbles are
+//           kept, so the final re-quantization costs nothing extra.
+
+#include "common.h"
+
+namespace {
+
+// Packed E2M1 codes of 16 weights at reciprocal scale R: two 32-bit words,
+// element 2k in the low nibble of byte k.  The hardware conversion rounds to
+// nearest even, saturates at 6 and keeps the sign (scale operand 1.0: no
+// extra scaling).
+__device__ __forceinline__ uint2 quantize_group(const float (&w)[kGroup], float R, uint2 old) {
+    // Every byte of both words is overwritten, so `old` only saves a move.
+    uint32_t p0 = old.x, p1 = old.y;
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[0] * R, w[1] * R, 1.0f, 0);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[2] * R, w[3] * R, 1.0f, 1);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[4] * R, w[5] * R, 1.0f, 2);
+    p0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p0, w[6] * R, w[7] * R, 1.0f, 3);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[8] * R, w[9] * R, 1.0f, 0);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[10] * R, w[11] * R, 1.0f, 1);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[12] * R, w[13] * R, 1.0f, 2);
+    p1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p1, w[14] * R, w[15] * R, 1.0f, 3);
+    return make_uint2(p0, p1);
+}
+
+// Adds the h-weighted squared residuals of elements 2K and 2K + 1 (byte K & 3
+// of word `src`) to the chains e[(2K) & 3] and e[(2K + 1) & 3].  Residuals
+// w - v S are single-rounding FMAs.
+template <int K>
+__device__ __forceinline__ void accumulate_pair(const float (&w)[kGroup], const float (&hh)[kGroup], uint32_t src,
+                                                float S, float (&e)[4]) {
+    const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, K & 3);
+    constexpr int j0 = 2 * K, j1 = 2 * K + 1;
+    const float r0 = fmaf(-v[0], S, w[j0]);
+    const float r1 = fmaf(-v[1], S, w[j1]);
+    e[j0 & 3] = fmaf(hh[j0] * r0, r0, e[j0 & 3]);
+    e[j1 & 3] = fmaf(hh[j1] * r1, r1, e[j1 & 3]);
+}
+
+// h-weighted squared error sum_j h_j (w_j - v_j S)^2 of a packed group: the
+// 16 terms go into 4 fp32 chains of 4 (j = q, q + 4, q + 8, q + 12),
+// combined as (e0 + e1) + (e2 + e3).
+__device__ __forceinline__ float group_error(const float (&w)[kGroup], const float (&hh)[kGroup], uint2 p,
+                                             float S) {
+    float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    accumulate_pair<0>(w, hh, p.x, S, e);
+    accumulate_pair<1>(w, hh, p.x, S, e);
+    accumulate_pair<2>(w, hh, p.x, S, e);
+    accumulate_pair<3>(w, hh, p.x, S, e);
+    accumulate_pair<4>(w, hh, p.y, S, e);
+    accumulate_pair<5>(w, hh, p.y, S, e);
+    accumulate_pair<6>(w, hh, p.y, S, e);
+    accumulate_pair<7>(w, hh, p.y, S, e);
+    return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+constexpr int kSearchThreads = 256;
+
+// How the walk's initial code c0 is chosen (values of the C ABI's init_mode).
+enum InitMode : int { kInitMaxAbs = 0, kInitFourOverSix = 1, kInitGiven = 2 };
+
+// Adds the squared residuals of elements 2K and 2K + 1 to the plain-error
+// chains (the 4over6 anchor score has no h).
+template <int K>
+__device__ __forceinline__ void accumulate_pair_plain(const float (&w)[kGroup], uint32_t src, float S,
+                                                      float (&e)[4]) {
+    const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(src, 1.0f, K & 3);
+    constexpr int j0 = 2 * K, j1 = 2 * K + 1;
+    const float r0 = fmaf(-v[0], S, w[j0]);
+    const float r1 = fmaf(-v[1], S, w[j1]);
+    e[j0 & 3] = fmaf(r0, r0, e[j0 & 3]);
+    e[j1 & 3] = fmaf(r1, r1, e[j1 & 3]);
+}
+
+// Plain squared error sum_j (w_j - v_j S)^2 of a packed group: single-rounding
+// residuals, 4 fp32 chains of 4.
+__device__ __forceinline__ float group_plain_error(const float (&w)[kGroup], uint2 p, float S) {
+    float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    accumulate_pair_plain<0>(w, p.x, S, e);
+    accumulate_pair_plain<1>(w, p.x, S, e);
+    accumulate_pair_plain<2>(w, p.x, S, e);
+    accumulate_pair_plain<3>(w, p.x, S, e);
+    accumulate_pair_plain<4>(w, p.y, S, e);
+    accumulate_pair_plain<5>(w, p.y, S, e);
+    accumulate_pair_plain<6>(w, p.y, S, e);
+    accumulate_pair_plain<7>(w, p.y, S, e);
+    return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+// Initial code of Eq. 7 from max|w| and an anchor (6 for max-abs; 4 or 6 for
+// 4over6): fp32(amax / anchor), then fp32(. / s_g), then Q_fp8 and the clip.
+__device__ __forceinline__ int anchor_code(float amax, float anchor, float s_g) {
+    const float s_init = amax / anchor;
+    return e4m3fn_code_clipped(s_init / s_g);
+}
+
+// Eq. 7 and 9-13 for one group held in registers: the initial code (by the
+// rule kInit; `given` is the caller's code for kInitGiven), then the walk
+// d = -down..up in pairs, keeping the first minimum.  With kStats it also
+// reports the chosen shift, its error and the error at d = 0.
+template <int kInit, bool kStats>
+__device__ __forceinline__ void search_group(const float (&w)[kGroup], const float (&hh)[kGroup],
+                                             const ScaleEntry *tab, int down, int up, float s_g, int given,
+                                             int &code, uint2 &best_p, int &shift, float &err_best,
+                                             float &err_init) {
+    int c0;
+    if (kInit == kInitGiven) {
+        c0 = min(max(given, 1), kMaxCode);
+    } else {
+        float amax = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
+        c0 = anchor_code(amax, 6.0f, s_g);
+        if (kInit == kInitFourOverSix) {
+            // Anchor 4 (amax / 4 is exact) against anchor 6 by plain squared
+            // error; anchor 4 on a tie.
+            const int c4 = anchor_code(amax, 4.0f, s_g);
+            const ScaleEntry e4 = tab[c4 + kTabPad];
+            const ScaleEntry e6 = tab[c0 + kTabPad];
+            const float l4 = group_plain_error(w, quantize_group(w, e4.R, make_uint2(0u, 0u)), e4.S);
+            const float l6 = group_plain_error(w, quantize_group(w, e6.R, make_uint2(0u, 0u)), e6.S);
+            if (l4 <= l6) c0 = c4;
+        }
+    }
+    const ScaleEntry *col = tab + (c0 + kTabPad);  // col[d] is candidate c0 + d, clipped
+    float best_e = 0.0f, e_init = 0.0f;
+    int best_d = -down;
+    best_p = make_uint2(0u, 0u);
+    // Scratch words the conversions rewrite in place (all 8 bytes each time),
+    // carried across iterations so no register copies are needed.
+    uint2 pa = best_p, pb = best_p;
+    int d = -down;
+    for (; d < up; d += 2) {
+        const ScaleEntry sa = col[d];
+        const ScaleEntry sb = col[d + 1];
+        pa = quantize_group(w, sa.R, pa);
+        pb = quantize_group(w, sb.R, pb);
+        const float ea = group_error(w, hh, pa, sa.S);
+        const float eb = group_error(w, hh, pb, sb.S);
+        if (kStats) {
+            if (d == 0) e_init = ea;
+            if (d + 1 == 0) e_init = eb;
+        }
+        if (d == -down || ea < best_e) {
+            best_e = ea;
+            best_d = d;
+            best_p = pa;
+        }
+        if (eb < best_e) {
+            best_e = eb;
+            best_d = d + 1;
+            best_p = pb;
+        }
+    }
+    if (d == up) {  // odd candidate count: the last one
+        const ScaleEntry se = col[d];
+        pa = quantize_group(w, se.R, pa);
+        const float e = group_error(w, hh, pa, se.S);
+        if (kStats && d == 0) e_init = e;
+        if (d == -down || e < best_e) {
+            best_e = e;
+            best_d = d;
+            best_p = pa;
+        }
+    }
+    code = min(max(c0 + best_d, 1), kMaxCode);
+    shift = best_d;
+    err_best = best_e;
+    err_init = e_init;
+}
+
+// Arguments of a search over a block of `rows` x (16 Gc) weights inside
+// larger row-major arrays.  Group (r, i) reads W at r * ldw + 16 i bf16
+// elements (ldw_vec counts 16-byte vectors), h at 16 i, the initial code at
+// r * ldi + i, and writes its code at r * ldc + i and its packed nibbles at
+// r * ldp + 8 i bytes (ldp_vec counts 8-byte words).
+struct SearchArgs {
+    const u32x4 *W;
+    uint64_t ldw_vec;
+    const float4 *h;
+    uint32_t num_groups;  // rows * Gc
+    uint32_t Gc;          // groups per row
+    int down, up;
+    float s_g;
+    const uint8_t *init;
+    uint64_t ldi;
+    uint8_t *codes;
+    uint64_t ldc;
+    uint2 *packed;
+    uint64_t ldp_vec;
+    int8_t *shift;    // statistics, [rows * Gc] at index g (kStats only)
+    float *err_best;
+    float *err_init;
+};
+
+// One group per lane over the flat index g = r * Gc + i of the block, so the
+// lanes of a wave cover consecutive groups of a row (contiguous loads and
+// stores) and a lane's h slice is h[16 i .. 16 i + 15].  A launch normally
+// covers every group once; larger problems loop with a grid stride.
+template <int kInit, bool kStats>
+__global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs a) {
+    __shared__ ScaleEntry tab[kTabSize];
+    __shared__ ScaleEntry uniq[kMaxCode + 1];
+    build_scale_table(tab, uniq, a.s_g);
+
+    const uint32_t stride = gridDim.x * kSearchThreads;
+    const uint32_t first = blockIdx.x * kSearchThreads;  // wave-uniform
+    uint32_t g = first + threadIdx.x;
+    if (g >= a.num_groups) return;
+    // (r, i) of g from the uniform block offset: at most one wrap per row
+    // crossed inside the block.
+    uint32_t r = first / a.Gc;
+    uint32_t i = first % a.Gc + threadIdx.x;
+    while (i >= a.Gc) {
+        i -= a.Gc;
+        ++r;
+    }
+    const uint32_t step_r = stride / a.Gc, step_i = stride % a.Gc;
+
+    for (;;) {
+        float w[kGroup];
+        const u32x4 *src = a.W + (uint64_t)r * a.ldw_vec + 2 * (uint64_t)i;
+        load_group(src, 0, w);
+        float hh[kGroup];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = a.h[4 * (uint64_t)i + q];
+            hh[4 * q] = v.x;
+            hh[4 * q + 1] = v.y;
+            hh[4 * q + 2] = v.z;
+            hh[4 * q + 3] = v.w;
+        }
+        const int given = kInit == kInitGiven ? (int)a.init[(uint64_t)r * a.ldi + i] : 0;
+        int code, shift;
+        uint2 best_p;
+        float e_best, e_init;
+        search_group<kInit, kStats>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p, shift, e_best, e_init);
+        a.codes[(uint64_t)r * a.ldc + i] = (uint8_t)code;
+        a.packed[(uint64_t)r * a.ldp_vec + i] = best_p;
+        if (kStats) {
+            a.shift[g] = (int8_t)shift;
+            a.err_best[g] = e_best;
+            a.err_init[g] = e_init;
+        }
+
+        if (a.num_groups - g <= stride) break;
+        g += stride;
+        r += step_r;
+        i += step_i;
+        if (i >= a.Gc) {
+            i -= a.Gc;
+            ++r;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *__restrict__ W,
+                                                                  int64_t num_groups, float s_g,
+                                                                  const uint8_t *__restrict__ codes,
+                                                                  uint2 *__restrict__ packed) {
+    __shared__ ScaleEntry tab[kTabSize];
+    __shared__ ScaleEntry uniq[kMaxCode + 1];
+    build_scale_table(tab, uniq, s_g);
+    const int64_t stride = (int64_t)gridDim.x * kSearchThreads;
+    for (int64_t g = (int64_t)blockIdx.x * kSearchThreads + threadIdx.x; g < num_groups; g += stride) {
+        float w[kGroup];
+        load_group(W, g, w);
+        const int c = min(max((int)codes[g], 1), kMaxCode);
+        packed[g] = quantize_group(w, tab[c + kTabPad].R, make_uint2(0u, 0u));
+    }
+}
+
+int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
+                 float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, uint8_t *codes, int64_t ldc,
+                 uint8_t *packed, int64_t ldp, hipStream_t stream, int8_t *shift = nullptr,
+                 float *err_best = nullptr, float *err_init = nullptr) {
+    const bool stats = shift || err_best || err_init;
+    if (out < 0 || cols < 0 || cols % kGroup != 0) return HSCALE_ERR_SHAPE;
+    const int64_t Gc = cols / kGroup;
+    if (out > 0 && cols > 0 && out > kMaxGroups / Gc) return HSCALE_ERR_SHAPE;
+    if (init_mode < kInitMaxAbs || init_mode > kInitGiven) return HSCALE_ERR_SHAPE;
+    if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
+    if (!scale_ok(s_g)) return HSCALE_ERR_SCALE;
+    if (out == 0 || cols == 0) return HSCALE_OK;
+    if (ldw < cols || ldc < Gc || ldp < cols / 2 || (init_mode == kInitGiven && ldi < Gc)) return HSCALE_ERR_SHAPE;
+    if (!W || !h || !codes || !packed || (init_mode == kInitGiven && !init_codes)) return HSCALE_ERR_NULL;
+    if (stats && (!shift || !err_best || !err_init)) return HSCALE_ERR_NULL;
+    if (!aligned(W, 16) || ldw % 8 != 0 || !aligned(h, 16) || !aligned(packed, 8) || ldp % 8 != 0)
+        return HSCALE_ERR_ALIGN;
+    if (stats && (!aligned(err_best, 4) || !aligned(err_init, 4))) return HSCALE_ERR_ALIGN;
+    const size_t nw = span(out, ldw, cols, 2), nh = (size_t)cols * 4;
+    const size_t nc = span(out, ldc, Gc, 1), np = span(out, ldp, cols / 2, 1);
+    if (overlaps(codes, nc, W, nw) || overlaps(codes, nc, h, nh) || overlaps(packed, np, W, nw) ||
+        overlaps(packed, np, h, nh) || overlaps(codes, nc, packed, np))
+        return HSCALE_ERR_OVERLAP;
+    if (init_mode == kInitGiven) {
+        // The codes may be refined in place (init_codes == scale_codes with
+        // the same stride: each group reads its own byte before writing it).
+        const size_t ni = span(out, ldi, Gc, 1);
+        const bool in_place = init_codes == codes && ldi == ldc;
+        if ((!in_place && overlaps(init_codes, ni, codes, nc)) || overlaps(init_codes, ni, packed, np))
+            return HSCALE_ERR_OVERLAP;
+    }
+    if (stats) {
+        // Every statistics array is written: none may overlap another buffer.
+        const size_t groups = (size_t)out * (size_t)Gc;
+        const struct {
+            const void *p;
+            size_t n;
+        } in_bufs[] = {{W, nw}, {h, nh}, {codes, nc}, {packed, np},
+                       {init_codes, init_mode == kInitGiven ? span(out, ldi, Gc, 1) : 0}},
+          st[] = {{shift, groups}, {err_best, groups * 4}, {err_init, groups * 4}};
+        for (const auto &a : st) {
+            for (const auto &b : in_bufs)
+                if (b.n && overlaps(a.p, a.n, b.p, b.n)) return HSCALE_ERR_OVERLAP;
+        }
+        if (overlaps(shift, groups, err_best, groups * 4) || overlaps(shift, groups, err_init, groups * 4) ||
+            overlaps(err_best, groups * 4, err_init, groups * 4))
+            return HSCALE_ERR_OVERLAP;
+    }
+    SearchArgs a;
+    a.W = static_cast<const u32x4 *>(W);
+    a.ldw_vec = (uint64_t)ldw / 8;
+    a.h = reinterpret_cast<const float4 *>(h);
+    a.num_groups = (uint32_t)(out * Gc);
+    a.Gc = (uint32_t)Gc;
+    a.down = down;
+    a.up = up;
+    a.s_g = s_g;
+    a.init = init_codes;
+    a.ldi = (uint64_t)ldi;
+    a.codes = codes;
+    a.ldc = (uint64_t)ldc;
+    a.packed = reinterpret_cast<uint2 *>(packed);
+    a.ldp_vec = (uint64_t)ldp / 8;
+    a.shift = shift;
+    a.err_best = err_best;
+    a.err_init = err_init;
+    const dim3 grid(grid_for(out * Gc, kSearchThreads)), block(kSearchThreads);
+    if (!stats) {
+        switch (init_mode) {
+            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, false>), grid, block, 0, stream, a); break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, false>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, false>), grid, block, 0, stream, a); break;
+        }
+    } else {
+        switch (init_mode) {
+            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, true>), grid, block, 0, stream, a); break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, true>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, true>), grid, block, 0, stream, a); break;
+        }
+    }
+    return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+int hscale_search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down,
+                        int32_t up, float global_scale, int32_t init_mode, const uint8_t *init_codes, int64_t ldi,
+                        uint8_t *scale_codes, int64_t ldc, uint8_t *packed_e2m1, int64_t ldp, hipStream_t stream) {
+    return search_block(W, ldw, out, cols, h, down, up, global_scale, init_mode, init_codes, ldi, scale_codes, ldc,
+                        packed_e2m1, ldp, stream);
+}
+
+int hscale_search_du(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                     float global_scale, uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitMaxAbs, nullptr, 0, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream);
+}
+
+int hscale_search(const void *W, int64_t out, int64_t in, const float *h, int32_t window, float global_scale,
+                  uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    return hscale_search_du(W, out, in, h, window, window, global_scale, scale_codes, packed_e2m1, stream);
+}
+
+int hscale_search_4over6(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                         float global_scale, uint8_t *scale_codes, uint8_t *packed_e2m1, hipStream_t stream) {
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitFourOverSix, nullptr, 0, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream);
+}
+
+int hscale_search_from(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                       float global_scale, const uint8_t *init_codes, uint8_t *scale_codes, uint8_t *packed_e2m1,
+                       hipStream_t stream) {
+    return search_block(W, in, out, in, h, down, up, global_scale, kInitGiven, init_codes, in / kGroup,
+                        scale_codes, in / kGroup, packed_e2m1, in / 2, stream);
+}
+
+int hscale_search_stats(const void *W, int64_t out, int64_t in, const float *h, int32_t down, int32_t up,
+                        float global_scale, int32_t init_mode, const uint8_t *init_codes, uint8_t *scale_codes,
+                        uint8_t *packed_e2m1, int8_t *shift, float *err_best, float *err_init, hipStream_t stream) {
+    if (out > 0 && in > 0 && (!shift || !err_best || !err_init)) return HSCALE_ERR_NULL;
+    return search_block(W, in, out, in, h, down, up, global_scale, init_mode, init_codes, in / kGroup, scale_codes,
+                        in / kGroup, packed_e2m1, in / 2, stream, shift, err_best, err_init);
+}
+
+int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,
+                    uint8_t *packed_e2m1, hipStream_t stream) {
+    if (out < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
+    if (out > 0 && in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
+    if (!scale_ok(global_scale)) return HSCALE_ERR_SCALE;
+    if (out == 0 || in == 0) return HSCALE_OK;
+    if (!W || !scale_codes || !packed_e2m1) return HSCALE_ERR_NULL;
+    if (!aligned(W, 16) || !aligned(packed_e2m1, 8)) return HSCALE_ERR_ALIGN;
+    const size_t nw = (size_t)out * (size_t)in * 2, nc = (size_t)out * (size_t)(in / kGroup);
+    const size_t np = (size_t)out * (size_t)(in / 2);
+    if (overlaps(packed_e2m1, np, W, nw) || overlaps(packed_e2m1, np, scale_codes, nc)) return HSCALE_ERR_OVERLAP;
+    const int64_t groups = out * (in / kGroup);
+    hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(groups, kSearchThreads)), dim3(kSearchThreads), 0, stream,
+                       static_cast<const u32x4 *>(W), groups, global_scale, scale_codes,
+                       reinterpret_cast<uint2 *>(packed_e2m1));
+    return launch_status();
+}
+
+}  // extern "C"
