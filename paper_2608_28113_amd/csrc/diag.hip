@@ -177,11 +177,13 @@ constexpr int kLfBN = 256;
 constexpr int kLfWM = 2;
 constexpr int kLfWN = 4;
 constexpr int kLfBK = 32;  // k per LDS stage (two 16-deep MFMA steps)
-constexpr int kLfThreads = 64 * kLfWM * kLfWN;
+constexpr int kLfThreads = 64 * kLfWM * kLfWN;  // two waves per SIMD (launch bounds): 256 registers each
 constexpr int kLfMI = kLfBM / kLfWM / 32;  // accumulator tiles per wave, token direction
 constexpr int kLfNJ = kLfBN / kLfWN / 32;  // accumulator tiles per wave, weight-row direction
 constexpr int kLfRows = kLfBM + 2 * kLfBN;  // LDS rows of 64 bytes per stage (X, dW hi, dW lo)
 constexpr int kLfStages = 3;                // LDS ring depth: two stages in flight while one is used
+constexpr int kLfAhead = kLfStages - 1;     // stages issued ahead of the one being read
+static_assert(kLfStages == 2 || kLfStages == 3, "the vmcnt waits below cover one or two stages ahead");
 constexpr int kLfWaves = kLfThreads / 64;
 constexpr int kLfDmaPerWave = kLfRows / 16 / kLfWaves;  // 1 KB direct-to-LDS loads per wave per stage
 static_assert(kLfRows % (16 * kLfWaves) == 0 && kLfBM % 16 == 0 && kLfBN % 16 == 0, "stage split");
@@ -270,7 +272,7 @@ struct LfArgs {
     const u32x4 *zero;  // 16 zero bytes, read for chunks outside X
 };
 
-__global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) {
+__global__ __launch_bounds__(kLfThreads, 2) void lfull_tile_kernel(const LfArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLfStages][kLfRows * 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % kLfWM, wn = wave / kLfWM;
@@ -315,22 +317,23 @@ __global__ __launch_bounds__(kLfThreads) void lfull_tile_kernel(const LfArgs a) 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    // Ring of kLfStages buffers: stage s + 2 is issued once every wave has
-    // finished reading stage s - 1 (the barrier), into that stage's buffer.
-    // Each wave first waits for its own loads of stage s (vmcnt counts them in
-    // issue order; the kLfDmaPerWave loads of stage s + 1 may stay in
-    // flight); the barrier then makes all of stage s visible.  A plain
-    // s_barrier is used: __syncthreads() adds a release fence that waits for
-    // every outstanding load, stage s + 1's included.
-    issue(0, 0);
-    if (stages > 1) issue(1, 1);
+    // Ring of kLfStages buffers, kLfAhead = kLfStages - 1 stages ahead: stage
+    // s + kLfAhead is issued once every wave has finished reading stage s - 1
+    // (the barrier), into that stage's buffer.  Each wave first waits for its
+    // own loads of stage s (vmcnt counts them in issue order; the loads of
+    // the later stages may stay in flight); the barrier then makes all of
+    // stage s visible.  A plain s_barrier is used: __syncthreads() adds a
+    // release fence that waits for every outstanding load.
+#pragma unroll
+    for (int p = 0; p < kLfAhead; ++p)
+        if (p < stages) issue(p, p);
     for (int s = 0; s < stages; ++s) {
-        if (s + 1 < stages)
+        if (kLfAhead > 1 && s + 1 < stages)
             __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLfDmaPerWave));
         else
             __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
         asm volatile("s_barrier" ::: "memory");
-        if (s + 2 < stages) issue(s + 2, (s + 2) % kLfStages);
+        if (s + kLfAhead < stages) issue(s + kLfAhead, (s + kLfAhead) % kLfStages);
         const uint8_t *base = lds[s % kLfStages];
 #pragma unroll
         for (int kk = 0; kk < kLfBK / 16; ++kk) {
