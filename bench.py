@@ -46,15 +46,33 @@ SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
 HERE = os.path.dirname(os.path.abspath(__file__))
 # Sources of the hot-path kernels (hdiag, search): the committed HBM-traffic
 # figures are valid only for the source they were measured on.
-HOT_SOURCES = [os.path.join(HERE, "paper_2608_28113_amd", "csrc", f) for f in ("common.h", "hdiag.hip", "search.hip")]
+HOT_SOURCES = ("common.h", "hdiag.hip", "search.hip")
+DIAG_SOURCES = ("common.h", "diag.hip")
 
 
-def hot_source_hash() -> str:
+def source_hash(names=HOT_SOURCES) -> str:
     h = hashlib.sha256()
-    for path in HOT_SOURCES:
-        with open(path, "rb") as f:
+    for name in names:
+        with open(os.path.join(HERE, "paper_2608_28113_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def diag_traffic(workload: str):
+    """HBM bytes of one output-error call (dW split + tile kernel) from the
+    committed rocprofv3 summary, or None when absent or stale."""
+    path = os.path.join(HERE, "profiles", f"output_error_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        prof = json.load(f)
+    if prof.get("kernel_source_sha256_16") != source_hash(DIAG_SOURCES):
+        return None
+    t = prof.get("traffic", {})
+    names = ("delta_split_kernel", "lfull_tile_kernel")
+    if not all(n in t for n in names):
+        return None
+    return sum(t[n]["read_bytes"] + t[n]["write_bytes"] for n in names), os.path.relpath(path, HERE)
 
 
 def search_ops_per_weight(K: int, init: str) -> int:
@@ -78,7 +96,7 @@ def measured_traffic(workload: str):
         return None
     with open(path) as f:
         prof = json.load(f)
-    if prof.get("kernel_source_sha256_16") != hot_source_hash():
+    if prof.get("kernel_source_sha256_16") != source_hash(HOT_SOURCES):
         return None
     t = prof.get("traffic", {})
 
@@ -353,6 +371,8 @@ def diag_leg(args, acts, layers, repeats=5):
     L_init = float(lfull(c0, p0).sum().item())
     flops = 2.0 * T * n * m
     tf = flops / (t_lf * 1e-3) / 1e12
+    traffic = diag_traffic(args.workload) if (args.workload, down, up, args.init) == ("down_proj", 4, 4, "maxabs") \
+        else None
     return {
         "layer": lname, "window": [down, up], "init": args.init, "tokens": T,
         "shift_fractions": {"keep": round(float(frac[down]), 4), "larger": round(float(frac[down + 1:].sum()), 4),
@@ -364,7 +384,8 @@ def diag_leg(args, acts, layers, repeats=5):
         "search_stats_ms": round(t_stats, 4), "shift_summary_ms": round(t_summ, 4),
         "output_error_ms": round(t_lf, 3),
         "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": traffic[0] if traffic else None,
+                     "traffic_source": traffic[1] if traffic else None,
                      "kernel": "hscale_output_error (delta_split_kernel + lfull_tile_kernel + hdiag_tree)",
                      "algorithmic_flops": flops, "issued_mfma_flops": 2 * flops},
     }
