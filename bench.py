@@ -119,9 +119,9 @@ def parse():
     ap.add_argument("--down", type=int, default=None, help="asymmetric shift set -down..+up")
     ap.add_argument("--up", type=int, default=None)
     ap.add_argument("--init", default="maxabs", choices=["maxabs", "4over6"])
-    ap.add_argument("--cpu-rows", type=int, default=1024,
+    ap.add_argument("--cpu-rows", type=int, default=3072,
                     help="rows of W in the CPU oracle sample (also checked for parity)")
-    ap.add_argument("--cpu-tokens", type=int, default=32768,
+    ap.add_argument("--cpu-tokens", type=int, default=65536,
                     help="tokens of X in the CPU oracle hdiag sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-diagnostics", action="store_true",
@@ -421,11 +421,11 @@ def cpu_leg(args, acts, layers):
     t_hd = time.perf_counter() - t0
     h_in = href.astype(np.float32)
     t0 = time.perf_counter()
-    oracle.search(Wb, h_in, s_g, down=down, up=up, init=init)
+    ref = oracle.search(Wb, h_in, s_g, down=down, up=up, init=init)
     t_search = time.perf_counter() - t0
     codes, packed = hs.search(W, torch.from_numpy(h_in).to(W.device), s_g, down=down, up=up, init=args.init)
     rep = parity.compare_search(Wb, h_in, s_g, down, up, codes[:rows].cpu().numpy(), packed[:rows].cpu().numpy(),
-                                init=init)
+                                init=init, oracle_result=ref)
     h_slice = hs.hdiag(X[:tok].contiguous()).cpu().numpy()
     hrep = parity.compare_h(h_slice, href)
     return {

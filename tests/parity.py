@@ -36,15 +36,17 @@ def compare_h(h_gpu: np.ndarray, h_ref: np.ndarray) -> dict:
 
 
 def compare_search(W_bits: np.ndarray, h32: np.ndarray, s_g: float, down: int, up: int,
-                   codes_gpu: np.ndarray, packed_gpu: np.ndarray, init="rtn") -> dict:
+                   codes_gpu: np.ndarray, packed_gpu: np.ndarray, init="rtn", oracle_result=None) -> dict:
     """``init`` is "rtn" (max-abs), "4over6" or an array of initial codes.
 
     For 4over6, a group whose two anchors' plain errors are within the
     near-tie band (and whose anchor codes differ) may start from either
-    anchor: its result is checked against the oracle's search from each."""
+    anchor: its result is checked against the oracle's search from each.
+    ``oracle_result`` is the oracle's search of the same inputs when the
+    caller already has it."""
     m, n = W_bits.shape
     G = n // 16
-    r = oracle.search(W_bits, h32, s_g, down=down, up=up, init=init)
+    r = oracle_result if oracle_result is not None else oracle.search(W_bits, h32, s_g, down=down, up=up, init=init)
     tie = oracle.near_tie_mask(r["e_best"], r["e_second"])
     codes_gpu = np.asarray(codes_gpu, np.uint8).reshape(m, G)
     packed_gpu = np.asarray(packed_gpu, np.uint8).reshape(m, n // 2)

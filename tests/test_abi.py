@@ -255,3 +255,16 @@ def test_output_error_validation(L):
     # empty problems add nothing (no pointer needed)
     assert L.hscale_output_error(0, 0, n, 0, m, 1e-3, 0, 0, 0, 0, 0, 0) == 0
     assert L.hscale_output_error(0, T, n, 0, 0, 1e-3, 0, 0, 0, 0, 0, 0) == 0
+
+
+def test_torch_front_end_rejects_bad_tensors_diagnostics():
+    import torch
+    from paper_2608_28113_amd import ops
+    W = torch.zeros(4, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        ops.search_stats(W, torch.zeros(16), 1e-3, 4, 4)  # not on the GPU
+    with pytest.raises(ValueError):
+        ops.shift_summary(torch.zeros(4, dtype=torch.int8), torch.zeros(4), torch.zeros(4), 4, 4)
+    with pytest.raises(ValueError):
+        ops.output_error(torch.zeros(8, 16, dtype=torch.bfloat16), W, 1e-3, torch.zeros(4, 1, dtype=torch.uint8),
+                         torch.zeros(4, 8, dtype=torch.uint8))
