@@ -324,8 +324,9 @@ def diag_leg(args, acts, layers, repeats=5):
     """Quality diagnostics of the paper's appendix on the workload's last
     layer, outside the timed hot-path steps: the search with per-group
     statistics and their per-shift summary (selected-shift figure), and the
-    Eq. 3 layer-output error L_full of the max-abs codes and of the searched
-    codes (window-sweep metric).  The output-error kernel is timed with HIP
+    Eq. 3 layer-output error L_full of the initial codes, of the searched
+    codes and of the full-ladder search, with the share of the full-ladder
+    gain this window recovers (the window-sweep metric).  The output-error kernel is timed with HIP
     events on the stream it runs on and priced against the bf16 matrix-core
     peak with its algorithmic 2 T n m flops (it issues twice that: the
     rounding error enters as two bf16 parts)."""
@@ -369,6 +370,12 @@ def diag_leg(args, acts, layers, repeats=5):
     L_search = float(L_search.sum().item())
     c0, p0 = hs.search(W, h, s_g, window=0, init=args.init, stream=stream)
     L_init = float(lfull(c0, p0).sum().item())
+    # The window sweep's score (App. "Candidate-Window Width"): the share of
+    # the max-abs -> full-ladder L_full gain that this window recovers; the
+    # full ladder is every positive E4M3 code (window 125 from any start).
+    cf, pf = hs.search(W, h, s_g, window=125, init=args.init, stream=stream)
+    L_full_grid = float(lfull(cf, pf).sum().item())
+    gain = L_init - L_full_grid
     flops = 2.0 * T * n * m
     tf = flops / (t_lf * 1e-3) / 1e12
     traffic = diag_traffic(args.workload) if (args.workload, down, up, args.init) == ("down_proj", 4, 4, "maxabs") \
@@ -379,8 +386,9 @@ def diag_leg(args, acts, layers, repeats=5):
                             "smaller": round(float(frac[:down].sum()), 4)},
         "shift_histogram": {str(d): int(c) for d, c in zip(range(-down, up + 1), count)},
         "surrogate_error_removed": round(float(1.0 - sb.sum() / si.sum()), 4),
-        "L_full_init": L_init, "L_full_search": L_search,
+        "L_full_init": L_init, "L_full_search": L_search, "L_full_full_grid": L_full_grid,
         "L_full_reduction": round(1.0 - L_search / L_init, 4),
+        "full_grid_gain_recovered": round((L_init - L_search) / gain, 4) if gain > 0 else None,
         "search_stats_ms": round(t_stats, 4), "shift_summary_ms": round(t_summ, 4),
         "output_error_ms": round(t_lf, 3),
         "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -306,3 +306,22 @@ def test_block_layers_small_windows(hs):
                                         packed.index_select(0, rows_t).cpu().numpy())
             print(f"[block {name} w={win}] near_ties={rep['near_ties']} mismatches={rep['mismatches']}", flush=True)
             assert rep["ok"]
+
+
+@pytest.mark.parametrize("down,up", [(9, 6), (8, 7), (8, 8), (12, 11), (12, 12), (15, 0), (0, 15)])
+def test_search_class_walk_paths(hs, down, up):
+    """Windows of 16..24 candidates walk the residue classes c mod 8 when
+    every lane of a wave has only normal, unclipped candidates; a wave with
+    one lane near either end of the ladder takes the plain walk.  Both must
+    equal the oracle."""
+    rng = np.random.default_rng(down * 31 + up)
+    m, n = 64, 1024  # 64 groups per row: one wave per row
+    w = (rng.standard_normal((m, n)) * 0.02).astype(np.float32)
+    w[5, 3] = 3.0        # row 5: one group with c0 at the top of the ladder
+    w[9, :16] *= 1e-3    # row 9: one group with a tiny c0
+    W = torch.from_numpy(w).to(torch.bfloat16)
+    h = torch.from_numpy(np.exp(rng.standard_normal(n)).astype(np.float32)).to(DEV)
+    s_g = harness_global_scale(W)
+    c0 = oracle.anchor_codes(tensor_bits(W), s_g, 6.0)
+    assert c0[5].max() == 126 and c0[9].min() < 8 + down
+    _assert_search_parity(hs, W.to(DEV), h, s_g, down, up, "class walk")
