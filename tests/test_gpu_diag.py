@@ -237,3 +237,24 @@ def test_output_error_full_size_sampled(hs):
     rows = np.unique(np.r_[np.random.default_rng(4).choice(wl.out, 10, replace=False), 0, wl.out - 1])
     ref = oracle.output_error(Xb, oracle.delta(Wb_all[rows], s_g, codes[rows], packed[rows]))
     _check_lfull(got.cpu().numpy()[rows], ref, "L_full down_proj sampled")
+
+
+def test_output_error_70b_shape_sampled(hs):
+    """The 70B down_proj shape (8192 x 28672: 32 row tiles, 896 k stages)
+    with 2048 calibration tokens; the stored tensor is seeded random codes
+    and nibbles (any stored NVFP4 tensor is a valid input); sampled rows
+    against the oracle."""
+    wl = CONFIGS["down_proj_70b"]
+    X = make_activations(wl, "cpu", tokens=2048)
+    Xb = tensor_bits(X)
+    W = make_weight(wl, DEV)
+    s_g = harness_global_scale(W)
+    rng = np.random.default_rng(6)
+    codes = rng.integers(60, 111, (wl.out, wl.inp // 16)).astype(np.uint8)
+    packed = rng.integers(0, 256, (wl.out, wl.inp // 2)).astype(np.uint8)
+    got = hs.output_error(X.to(DEV), W, s_g, torch.from_numpy(codes).to(DEV), torch.from_numpy(packed).to(DEV))
+    torch.cuda.synchronize()
+    rows = np.unique(np.r_[rng.choice(wl.out, 8, replace=False), 0, wl.out - 1])
+    Wb = tensor_bits(W[torch.from_numpy(rows).to(DEV)])
+    ref = oracle.output_error(Xb, oracle.delta(Wb, s_g, codes[rows], packed[rows]))
+    _check_lfull(got.cpu().numpy()[rows], ref, "L_full 70b sampled")
