@@ -18,6 +18,7 @@ constexpr int kSumThreads = 256;
 constexpr int kSumPerThread = 16;
 constexpr int kSumChunk = kSumThreads * kSumPerThread;
 constexpr int kSumOutside = 1 << 20;  // shift value standing for "no group"
+static_assert(kSumThreads == 256, "the block reductions below combine exactly four waves");
 
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(64) void shift_summary_final(const double *__restri
 // dW is formed once in fp32 (w - v S[c], one rounding) and split into two
 // bf16 planes hi + lo (|dW - hi - lo| <= 2^-18 |dW|), so X dW^T is two bf16
 // MFMA products accumulated in fp32.  Each block computes a 256-token x
-// 128-row tile of X dW^T in registers and reduces the squares of its columns
+// 256-row tile of X dW^T in registers and reduces the squares of its columns
 // in fp64; the tile is never written.  Per-tile column sums go to a
 // workspace and a fixed-order tree adds them to row_err.
 // ---------------------------------------------------------------------------
@@ -269,7 +270,7 @@ struct LfArgs {
     int64_t out;      // weight rows
     int64_t ntiles;   // rows_pad / kLfBN
     double *partial;    // [token tiles of the pass, out]
-    const u32x4 *zero;  // 16 zero bytes, read for chunks outside X
+    const u32x4 *zero;  // zeros, read (16 bytes per lane) for chunks outside X
 };
 
 __global__ __launch_bounds__(kLfThreads, 2) void lfull_tile_kernel(const LfArgs a) {
@@ -404,7 +405,11 @@ LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
     p.rows_pad = (out + kLfBN - 1) / kLfBN * kLfBN;
     p.ntiles = p.rows_pad / kLfBN;
     const int64_t tiles = (tokens + kLfBM - 1) / kLfBM;
-    p.tiles_per_pass = tiles < kLfMaxTilesPerPass ? tiles : kLfMaxTilesPerPass;
+    // A pass launches tiles_per_pass x ntiles blocks: at most kLfMaxTilesPerPass
+    // token tiles, and never more blocks than a grid dimension holds.
+    const int64_t grid_cap = INT_MAX / p.ntiles > 0 ? INT_MAX / p.ntiles : 1;
+    const int64_t cap = grid_cap < kLfMaxTilesPerPass ? grid_cap : kLfMaxTilesPerPass;
+    p.tiles_per_pass = tiles < cap ? tiles : cap;
     p.plane_bytes = round_up((size_t)p.rows_pad * (size_t)p.ldd * 2, 256);
     p.zero_offset = 2 * p.plane_bytes;
     p.partial_offset = p.zero_offset + 256;
