@@ -60,6 +60,8 @@ MUTANTS = {
                                       "sum_rel[k] += (e_init[g] - e_best[g]) / e_best[g];"),
     "summary_swaps_sums": ("sum_init[k] += e_init[g];\n        sum_best[k] += e_best[g];",
                            "sum_init[k] += e_best[g];\n        sum_best[k] += e_init[g];"),
+    "stats_init_error_at_wrong_shift": ("if (d == 0 && e_init) *e_init = e;", "if (d == 1 && e_init) *e_init = e;"),
+    "delta_code_off_by_one": ("int c = codes[r * G + j / 16];", "int c = codes[r * G + j / 16] + 1;"),
     "stats_shift_not_first_min": ("            best_c = c;\n            best_d = d;",
                                   "            best_c = c;\n            best_d = d - (d > 0);"),
 }
