@@ -26,35 +26,60 @@ constexpr int kGroup = 16;
 constexpr int kMaxCode = 126;  // positive finite E4M3FN codes are 1..126
 constexpr int kMaxWindow = 125;
 
-constexpr int kTreeCols = 64;
-constexpr int kTreeLanes = 4;
+constexpr int kTreeThreads = 256;
 
-// Sums the slice partials of each column in a fixed order: lane q of a
-// column adds slices q, q + 4, ...; the four lane sums combine as
-// ((s0 + s1) + s2) + s3.  kAccumulate adds the sum to an fp64 accumulator
-// instead of writing fp32 h.
-template <bool kAccumulate>
-__global__ __launch_bounds__(kTreeCols *kTreeLanes) void hdiag_tree(const double *__restrict__ partial,
-                                                                     int64_t slices, int64_t in,
-                                                                     float *__restrict__ h,
-                                                                     double *__restrict__ h64) {
-    const int lane = threadIdx.x % kTreeCols;
-    const int q = threadIdx.x / kTreeCols;
-    const int64_t col = (int64_t)blockIdx.x * kTreeCols + lane;
+// Sums the slice partials of each column in a fixed order: kLanes lanes per
+// column, lane q adding slices q, q + kLanes, ... in order, then the lane
+// sums added in lane order.  kAccumulate adds the sum to an fp64 accumulator
+// instead of writing fp32 h.  The lane count is chosen from the slice count
+// alone (tree_lanes), so a given problem always sums in the same order.
+template <bool kAccumulate, int kLanes>
+__global__ __launch_bounds__(kTreeThreads) void hdiag_tree(const double *__restrict__ partial, int64_t slices,
+                                                           int64_t in, float *__restrict__ h,
+                                                           double *__restrict__ h64) {
+    constexpr int kCols = kTreeThreads / kLanes;
+    const int lane = threadIdx.x % kCols;
+    const int q = threadIdx.x / kCols;
+    const int64_t col = (int64_t)blockIdx.x * kCols + lane;
     double s = 0.0;
     if (col < in) {
-        for (int64_t k = q; k < slices; k += kTreeLanes) s += partial[k * in + col];
+#pragma unroll 8
+        for (int64_t k = q; k < slices; k += kLanes) s += partial[k * in + col];
     }
-    __shared__ double red[kTreeLanes][kTreeCols];
+    __shared__ double red[kLanes][kCols];
     red[q][lane] = s;
     __syncthreads();
     if (q == 0 && col < in) {
-        const double total = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+        double total = red[0][lane];
+#pragma unroll
+        for (int l = 1; l < kLanes; ++l) total += red[l][lane];
         if (kAccumulate)
             h64[col] += total;
         else
             h[col] = (float)total;
     }
+}
+
+// Lanes per column for summing `slices` partials: about 16 or fewer slices
+// per lane, so the per-lane chains stay short and small column counts still
+// spread over many blocks.
+inline int tree_lanes(int64_t slices) { return slices <= 64 ? 4 : slices <= 256 ? 16 : 64; }
+
+// Launches the fixed-order column sum of slices x in partials.
+template <bool kAccumulate>
+inline void launch_tree(const double *partial, int64_t slices, int64_t in, float *h, double *h64,
+                        hipStream_t stream) {
+    const int lanes = tree_lanes(slices);
+    const unsigned blocks = (unsigned)((in + kTreeThreads / lanes - 1) / (kTreeThreads / lanes));
+    if (lanes == 4)
+        hipLaunchKernelGGL((hdiag_tree<kAccumulate, 4>), dim3(blocks), dim3(kTreeThreads), 0, stream, partial, slices,
+                           in, h, h64);
+    else if (lanes == 16)
+        hipLaunchKernelGGL((hdiag_tree<kAccumulate, 16>), dim3(blocks), dim3(kTreeThreads), 0, stream, partial,
+                           slices, in, h, h64);
+    else
+        hipLaunchKernelGGL((hdiag_tree<kAccumulate, 64>), dim3(blocks), dim3(kTreeThreads), 0, stream, partial,
+                           slices, in, h, h64);
 }
 
 // ---------------------------------------------------------------------------

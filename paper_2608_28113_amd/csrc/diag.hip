@@ -513,7 +513,6 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
                        reinterpret_cast<u32x4 *>(ws + p.zero_offset));
     if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
     const int64_t pass_tokens = p.tiles_per_pass * kLfBM;
-    const unsigned tree_blocks = (unsigned)((out + kTreeCols - 1) / kTreeCols);
     for (int64_t t0 = 0; t0 < tokens; t0 += pass_tokens) {
         LfArgs a;
         a.tokens = tokens - t0 < pass_tokens ? tokens - t0 : pass_tokens;
@@ -529,8 +528,7 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
         const int64_t tiles = (a.tokens + kLfBM - 1) / kLfBM;
         hipLaunchKernelGGL(lfull_tile_kernel, dim3((unsigned)(tiles * p.ntiles)), dim3(kLfThreads), 0, stream, a);
         if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
-        hipLaunchKernelGGL(hdiag_tree<true>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
-                           static_cast<const double *>(partial), tiles, out, (float *)nullptr, row_err);
+        launch_tree<true>(partial, tiles, out, nullptr, row_err, stream);
         if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
     }
     return HSCALE_OK;

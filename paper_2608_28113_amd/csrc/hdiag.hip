@@ -9,7 +9,7 @@
 //                  and one fp64 partial per (slice, column) goes to the
 //                  caller's workspace.
 //   hdiag_tree     fixed-order fp64 sum of the slice partials, one fp32 h per
-//                  column.  No atomics: results are bit-identical run to run.
+//                  column (4, 16 or 64 lanes per column by slice count).  No atomics: results are bit-identical run to run.
 
 #include "common.h"
 
@@ -163,13 +163,10 @@ int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, 
     } else if (accumulate) {
         return HSCALE_OK;  // nothing to add
     }
-    const unsigned tree_blocks = (unsigned)((in + kTreeCols - 1) / kTreeCols);
     if (accumulate)
-        hipLaunchKernelGGL(hdiag_tree<true>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
-                           static_cast<const double *>(workspace), p.slices, in, (float *)nullptr, h64);
+        launch_tree<true>(static_cast<const double *>(workspace), p.slices, in, nullptr, h64, stream);
     else
-        hipLaunchKernelGGL(hdiag_tree<false>, dim3(tree_blocks), dim3(kTreeCols * kTreeLanes), 0, stream,
-                           static_cast<const double *>(workspace), p.slices, in, h, (double *)nullptr);
+        launch_tree<false>(static_cast<const double *>(workspace), p.slices, in, h, nullptr, stream);
     return launch_status();
 }
 
