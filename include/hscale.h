@@ -33,7 +33,9 @@
  *     nothing is launched.  Kernel faults surface at the caller's next sync.
  *   - bf16 tensors are passed as their 16-bit patterns, row-major.
  *   - Inputs must be finite (no NaN or Inf); outputs for non-finite inputs
- *     are unspecified.  Outputs must not overlap inputs.
+ *     are unspecified.  Outputs must not overlap inputs.  h is formed from
+ *     fp32 squares of bf16 activations, exact for |x| < 2^64; larger
+ *     activations overflow h to +Inf.
  *   - Number formats: E4M3 is OCP E4M3FN.  Scale code byte c in 1..126 is
  *     the positive finite E4M3FN value l_c (2^-9 .. 448).  E2M1 magnitudes
  *     are {0, 0.5, 1, 1.5, 2, 3, 4, 6}; a 4-bit code is sign << 3 | index.
