@@ -34,7 +34,7 @@
  *   - bf16 tensors are passed as their 16-bit patterns, row-major.
  *   - Inputs must be finite (no NaN or Inf); outputs for non-finite inputs
  *     are unspecified.  Outputs must not overlap inputs.  h is formed from
- *     fp32 squares of bf16 activations, exact for |x| < 2^64; larger
+ *     fp32 squares of bf16 activations, exact for 2^-63 <= |x| < 2^64; larger
  *     activations overflow h to +Inf.
  *   - Number formats: E4M3 is OCP E4M3FN.  Scale code byte c in 1..126 is
  *     the positive finite E4M3FN value l_c (2^-9 .. 448).  E2M1 magnitudes
