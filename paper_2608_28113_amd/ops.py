@@ -3,6 +3,11 @@
 PyTorch supplies device memory and the current stream; these functions only
 check tensor metadata, allocate outputs and pass raw pointers to
 libhscale.so.  All arithmetic happens in the library's HIP kernels.
+
+The C ABI cannot see buffer sizes or devices, so every tensor handed to it
+here (inputs, caller-provided outputs and workspaces) is checked for dtype,
+shape, contiguity and device first: a wrong buffer raises ValueError and
+nothing is launched.
 """
 from __future__ import annotations
 
@@ -23,9 +28,73 @@ def _stream(stream) -> int:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _bf16_matrix(t: torch.Tensor, name: str) -> None:
-    if t.dtype != torch.bfloat16 or t.dim() != 2 or not t.is_cuda or not t.is_contiguous():
+def _on_device(t) -> bool:
+    """t is a tensor in GPU memory (the only memory the kernels may touch)."""
+    return isinstance(t, torch.Tensor) and t.is_cuda
+
+
+def _bf16_matrix(t, name: str) -> None:
+    if (not _on_device(t) or t.dtype != torch.bfloat16 or t.dim() != 2 or not t.is_contiguous()):
         raise ValueError(f"{name} must be a contiguous 2-D bf16 CUDA tensor")
+
+
+def _tensor(t, name: str, dtype, shape, device) -> torch.Tensor:
+    """t must be a contiguous tensor of this dtype and shape on `device`."""
+    if (not isinstance(t, torch.Tensor) or t.dtype != dtype or tuple(t.shape) != tuple(shape)
+            or t.device != device or not t.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")
+    return t
+
+
+def _out(t, name: str, dtype, shape, device) -> torch.Tensor:
+    """A caller-provided output (checked) or a new one."""
+    if t is None:
+        return torch.empty(tuple(shape), dtype=dtype, device=device)
+    return _tensor(t, name, dtype, shape, device)
+
+
+def _workspace(ws, need: int, device) -> tuple[int, int]:
+    """(pointer, bytes) of a caller-provided scratch tensor (any dtype,
+    contiguous, on `device`) or of a new one; the library checks the size."""
+    if ws is None:
+        if need <= 0:
+            return 0, 0
+        ws = torch.empty(need, dtype=torch.uint8, device=device)
+    elif not isinstance(ws, torch.Tensor) or ws.device != device or not ws.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous tensor on {device}")
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def _row_view(t, dtype, shape, device, name: str) -> int:
+    """A 2-D view with unit column stride; returns its row stride."""
+    if (not isinstance(t, torch.Tensor) or t.dtype != dtype or t.dim() != 2 or tuple(t.shape) != tuple(shape)
+            or t.device != device or (t.shape[1] > 1 and t.stride(1) != 1)):
+        raise ValueError(f"{name} must be a 2-D {dtype} view of shape {tuple(shape)} on {device} "
+                         "with unit column stride")
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
+def _init_mode(init, shape, device):
+    """(init_mode, initial-code tensor or None) of an `init` argument."""
+    if isinstance(init, str):
+        modes = {"maxabs": _lib.HSCALE_INIT_MAXABS, "rtn": _lib.HSCALE_INIT_MAXABS,
+                 "4over6": _lib.HSCALE_INIT_4OVER6}
+        if init not in modes:
+            raise ValueError("init must be 'maxabs', '4over6' or a uint8 tensor of codes")
+        return modes[init], None
+    if isinstance(init, torch.Tensor):
+        return _lib.HSCALE_INIT_GIVEN, _tensor(init, "initial codes", torch.uint8, shape, device)
+    raise ValueError("init must be 'maxabs', '4over6' or a uint8 tensor of codes")
+
+
+def _window(window, down, up) -> tuple[int, int]:
+    if window is not None:
+        if down is not None or up is not None:
+            raise ValueError("give either window or down/up")
+        return int(window), int(window)
+    if down is None or up is None:
+        raise ValueError("give window or both down and up")
+    return int(down), int(up)
 
 
 def hdiag_workspace_bytes(tokens: int, in_features: int) -> int:
@@ -38,27 +107,11 @@ def hdiag(X: torch.Tensor, h: torch.Tensor | None = None, workspace: torch.Tenso
     """h = diag(X^T X) (Sec. 3.2, Eq. 4) of bf16 X [tokens, in] as fp32 [in]."""
     _bf16_matrix(X, "X")
     T, n = X.shape
-    if h is None:
-        h = torch.empty(n, dtype=torch.float32, device=X.device)
-    need = hdiag_workspace_bytes(T, n)
-    if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else 0
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    h = _out(h, "h", torch.float32, (n,), X.device)
+    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), X.device)
     _check(_lib.hscale_hdiag(X.data_ptr(), T, n, h.data_ptr(), ws_ptr, ws_bytes, _stream(stream)),
            "hscale_hdiag")
     return h
-
-
-def _init_mode(init):
-    if isinstance(init, str):
-        return {"maxabs": _lib.HSCALE_INIT_MAXABS, "rtn": _lib.HSCALE_INIT_MAXABS,
-                "4over6": _lib.HSCALE_INIT_4OVER6}[init], None
-    if isinstance(init, torch.Tensor):
-        if init.dtype != torch.uint8 or not init.is_cuda:
-            raise ValueError("initial codes must be a uint8 CUDA tensor")
-        return _lib.HSCALE_INIT_GIVEN, init
-    raise ValueError("init must be 'maxabs', '4over6' or a uint8 tensor of codes")
 
 
 def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | None = None,
@@ -74,41 +127,26 @@ def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | 
     """
     _bf16_matrix(W, "W")
     m, n = W.shape
-    if h.dtype != torch.float32 or h.shape != (n,) or not h.is_contiguous():
-        raise ValueError("h must be a contiguous fp32 tensor of shape [in]")
-    if window is not None:
-        if down is not None or up is not None:
-            raise ValueError("give either window or down/up")
-        down = up = int(window)
-    if down is None or up is None:
-        raise ValueError("give window or both down and up")
-    mode, init_t = _init_mode(init)
-    if scale_codes is None:
-        scale_codes = torch.empty((m, n // 16), dtype=torch.uint8, device=W.device)
-    if packed_e2m1 is None:
-        packed_e2m1 = torch.empty((m, n // 2), dtype=torch.uint8, device=W.device)
+    dev = W.device
+    _tensor(h, "h", torch.float32, (n,), dev)
+    down, up = _window(window, down, up)
+    mode, init_t = _init_mode(init, (m, n // 16), dev)
+    scale_codes = _out(scale_codes, "scale_codes", torch.uint8, (m, n // 16), dev)
+    packed_e2m1 = _out(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), dev)
     s = _stream(stream)
     if mode == _lib.HSCALE_INIT_MAXABS:
-        st = _lib.hscale_search_du(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale),
+        st = _lib.hscale_search_du(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
                                    scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_du")
     elif mode == _lib.HSCALE_INIT_4OVER6:
-        st = _lib.hscale_search_4over6(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up),
-                                       float(global_scale), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        st = _lib.hscale_search_4over6(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
+                                       scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_4over6")
     else:
-        if init_t.shape != (m, n // 16) or not init_t.is_contiguous():
-            raise ValueError("initial codes must be a contiguous uint8 tensor [out, in/16]")
-        st = _lib.hscale_search_from(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale),
+        st = _lib.hscale_search_from(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
                                      init_t.data_ptr(), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_from")
     return scale_codes, packed_e2m1
-
-
-def _row_view(t: torch.Tensor, dtype, name: str):
-    if t.dtype != dtype or t.dim() != 2 or not t.is_cuda or (t.shape[1] > 1 and t.stride(1) != 1):
-        raise ValueError(f"{name} must be a 2-D {dtype} CUDA tensor (view) with unit column stride")
-    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
 
 
 def search_block(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: int, up: int,
@@ -117,22 +155,20 @@ def search_block(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: in
     (bf16), h = hfull[a:b], scale_codes = codes[:, a/16:b/16] and
     packed_e2m1 = packed[:, a/2:b/2] (uint8), as in the paper's GPTQ
     combination (App. B).  Outputs are written in place."""
+    if not _on_device(W) or W.dim() != 2:
+        raise ValueError("W must be a 2-D bf16 CUDA view")
     m, cols = W.shape
-    ldw = _row_view(W, torch.bfloat16, "W")
-    ldc = _row_view(scale_codes, torch.uint8, "scale_codes")
-    ldp = _row_view(packed_e2m1, torch.uint8, "packed_e2m1")
-    if scale_codes.shape != (m, cols // 16) or packed_e2m1.shape != (m, cols // 2):
-        raise ValueError("output views do not match the block")
-    if h.dtype != torch.float32 or h.shape != (cols,) or not h.is_contiguous():
-        raise ValueError("h must be a contiguous fp32 slice of shape [cols]")
-    mode, init_t = _init_mode(init)
-    ldi = 0
-    iptr = 0
-    if init_t is not None:
-        ldi = _row_view(init_t, torch.uint8, "init codes")
-        if init_t.shape != (m, cols // 16):
-            raise ValueError("initial codes do not match the block")
-        iptr = init_t.data_ptr()
+    dev = W.device
+    ldw = _row_view(W, torch.bfloat16, (m, cols), dev, "W")
+    ldc = _row_view(scale_codes, torch.uint8, (m, cols // 16), dev, "scale_codes")
+    ldp = _row_view(packed_e2m1, torch.uint8, (m, cols // 2), dev, "packed_e2m1")
+    _tensor(h, "h", torch.float32, (cols,), dev)
+    if isinstance(init, torch.Tensor):
+        ldi = _row_view(init, torch.uint8, (m, cols // 16), dev, "initial codes")
+        mode, iptr = _lib.HSCALE_INIT_GIVEN, init.data_ptr()
+    else:
+        mode, _ = _init_mode(init, None, dev)
+        iptr, ldi = 0, 0
     st = _lib.hscale_search_block(W.data_ptr(), ldw, m, cols, h.data_ptr(), int(down), int(up),
                                   float(global_scale), mode, iptr, ldi, scale_codes.data_ptr(), ldc,
                                   packed_e2m1.data_ptr(), ldp, _stream(stream))
@@ -145,13 +181,8 @@ def hdiag_accumulate(X: torch.Tensor, h64: torch.Tensor, workspace: torch.Tensor
     """h64 += diag(X^T X) for one calibration batch (fp64 accumulator)."""
     _bf16_matrix(X, "X")
     T, n = X.shape
-    if h64.dtype != torch.float64 or h64.shape != (n,) or not h64.is_contiguous():
-        raise ValueError("h64 must be a contiguous fp64 tensor of shape [in]")
-    need = hdiag_workspace_bytes(T, n)
-    if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else 0
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _tensor(h64, "h64", torch.float64, (n,), X.device)
+    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), X.device)
     _check(_lib.hscale_hdiag_accumulate(X.data_ptr(), T, n, h64.data_ptr(), ws_ptr, ws_bytes,
                                         _stream(stream)), "hscale_hdiag_accumulate")
     return h64
@@ -159,9 +190,11 @@ def hdiag_accumulate(X: torch.Tensor, h64: torch.Tensor, workspace: torch.Tensor
 
 def hdiag_finalize(h64: torch.Tensor, h: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """h = fp32(h64)."""
+    if not _on_device(h64) or h64.dim() != 1:
+        raise ValueError("h64 must be a 1-D fp64 CUDA tensor")
     n = h64.shape[0]
-    if h is None:
-        h = torch.empty(n, dtype=torch.float32, device=h64.device)
+    _tensor(h64, "h64", torch.float64, (n,), h64.device)
+    h = _out(h, "h", torch.float32, (n,), h64.device)
     _check(_lib.hscale_hdiag_finalize(h64.data_ptr(), n, h.data_ptr(), _stream(stream)), "hscale_hdiag_finalize")
     return h
 
@@ -171,10 +204,8 @@ def quantize(W: torch.Tensor, global_scale: float, scale_codes: torch.Tensor,
     """Packed E2M1 codes of W at the given scale codes (final re-quantization)."""
     _bf16_matrix(W, "W")
     m, n = W.shape
-    if scale_codes.dtype != torch.uint8 or scale_codes.shape != (m, n // 16) or not scale_codes.is_contiguous():
-        raise ValueError("scale_codes must be a contiguous uint8 tensor [out, in/16]")
-    if packed_e2m1 is None:
-        packed_e2m1 = torch.empty((m, n // 2), dtype=torch.uint8, device=W.device)
+    _tensor(scale_codes, "scale_codes", torch.uint8, (m, n // 16), W.device)
+    packed_e2m1 = _out(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), W.device)
     _check(_lib.hscale_quantize(W.data_ptr(), m, n, float(global_scale), scale_codes.data_ptr(),
                                 packed_e2m1.data_ptr(), _stream(stream)), "hscale_quantize")
     return packed_e2m1
@@ -188,24 +219,19 @@ def search_stats(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: in
     and at shift 0)."""
     _bf16_matrix(W, "W")
     m, n = W.shape
-    if h.dtype != torch.float32 or h.shape != (n,) or not h.is_contiguous():
-        raise ValueError("h must be a contiguous fp32 tensor of shape [in]")
-    mode, init_t = _init_mode(init)
-    iptr = 0
-    if init_t is not None:
-        if init_t.shape != (m, n // 16) or not init_t.is_contiguous():
-            raise ValueError("initial codes must be a contiguous uint8 tensor [out, in/16]")
-        iptr = init_t.data_ptr()
+    dev = W.device
+    _tensor(h, "h", torch.float32, (n,), dev)
     G = (m, n // 16)
-    out = dict(scale_codes=torch.empty(G, dtype=torch.uint8, device=W.device),
-               packed_e2m1=torch.empty((m, n // 2), dtype=torch.uint8, device=W.device),
-               shift=torch.empty(G, dtype=torch.int8, device=W.device),
-               err_best=torch.empty(G, dtype=torch.float32, device=W.device),
-               err_init=torch.empty(G, dtype=torch.float32, device=W.device))
+    mode, init_t = _init_mode(init, G, dev)
+    out = dict(scale_codes=torch.empty(G, dtype=torch.uint8, device=dev),
+               packed_e2m1=torch.empty((m, n // 2), dtype=torch.uint8, device=dev),
+               shift=torch.empty(G, dtype=torch.int8, device=dev),
+               err_best=torch.empty(G, dtype=torch.float32, device=dev),
+               err_init=torch.empty(G, dtype=torch.float32, device=dev))
     st = _lib.hscale_search_stats(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale), mode,
-                                  iptr, out["scale_codes"].data_ptr(), out["packed_e2m1"].data_ptr(),
-                                  out["shift"].data_ptr(), out["err_best"].data_ptr(), out["err_init"].data_ptr(),
-                                  _stream(stream))
+                                  init_t.data_ptr() if init_t is not None else 0, out["scale_codes"].data_ptr(),
+                                  out["packed_e2m1"].data_ptr(), out["shift"].data_ptr(),
+                                  out["err_best"].data_ptr(), out["err_init"].data_ptr(), _stream(stream))
     _check(st, "hscale_search_stats")
     return out
 
@@ -215,13 +241,16 @@ def shift_summary(shift: torch.Tensor, err_best: torch.Tensor, err_init: torch.T
     """Per-shift counts and fp64 sums of initial errors, chosen errors and
     relative reductions over the groups (bins d = -down..up), as tensors of
     length down + up + 1 on the device."""
+    if not _on_device(shift):
+        raise ValueError("shift must be an int8 CUDA tensor")
     groups = shift.numel()
+    dev = shift.device
     for t, dt, name in ((shift, torch.int8, "shift"), (err_best, torch.float32, "err_best"),
                         (err_init, torch.float32, "err_init")):
-        if t.dtype != dt or not t.is_cuda or not t.is_contiguous() or t.numel() != groups:
-            raise ValueError(f"{name} must be a contiguous {dt} CUDA tensor with one entry per group")
+        if (not isinstance(t, torch.Tensor) or t.dtype != dt or t.device != dev or not t.is_contiguous()
+                or t.numel() != groups):
+            raise ValueError(f"{name} must be a contiguous {dt} tensor on {dev} with one entry per group")
     K = int(down) + int(up) + 1
-    dev = shift.device
     # counts are uint64 in the C ABI; int64 holds them (< 2^63) with full torch support
     out = dict(count=torch.empty(K, dtype=torch.int64, device=dev),
                sum_init=torch.empty(K, dtype=torch.float64, device=dev),
@@ -253,21 +282,15 @@ def output_error(X: torch.Tensor, W: torch.Tensor, global_scale: float, scale_co
     _bf16_matrix(W, "W")
     T, n = X.shape
     m = W.shape[0]
-    if W.shape[1] != n:
-        raise ValueError("X and W disagree on in_features")
-    if scale_codes.dtype != torch.uint8 or scale_codes.shape != (m, n // 16) or not scale_codes.is_contiguous():
-        raise ValueError("scale_codes must be a contiguous uint8 tensor [out, in/16]")
-    if packed_e2m1.dtype != torch.uint8 or packed_e2m1.shape != (m, n // 2) or not packed_e2m1.is_contiguous():
-        raise ValueError("packed_e2m1 must be a contiguous uint8 tensor [out, in/2]")
+    dev = X.device
+    if W.shape[1] != n or W.device != dev:
+        raise ValueError("X and W must share in_features and device")
+    _tensor(scale_codes, "scale_codes", torch.uint8, (m, n // 16), dev)
+    _tensor(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), dev)
     if row_err is None:
-        row_err = torch.zeros(m, dtype=torch.float64, device=X.device)
-    if row_err.dtype != torch.float64 or row_err.shape != (m,) or not row_err.is_contiguous():
-        raise ValueError("row_err must be a contiguous fp64 tensor [out]")
-    need = output_error_workspace_bytes(T, n, m)
-    if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else 0
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        row_err = torch.zeros(m, dtype=torch.float64, device=dev)
+    _tensor(row_err, "row_err", torch.float64, (m,), dev)
+    ws_ptr, ws_bytes = _workspace(workspace, output_error_workspace_bytes(T, n, m), dev)
     _check(_lib.hscale_output_error(X.data_ptr(), T, n, W.data_ptr(), m, float(global_scale),
                                     scale_codes.data_ptr(), packed_e2m1.data_ptr(), row_err.data_ptr(), ws_ptr,
                                     ws_bytes, _stream(stream)), "hscale_output_error")
