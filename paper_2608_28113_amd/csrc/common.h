@@ -15,6 +15,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <type_traits>
 
 #include "hscale.h"
 
@@ -134,15 +135,18 @@ __device__ __forceinline__ void build_scale_table(ScaleEntry *tab, ScaleEntry *u
     __syncthreads();
 }
 
-__device__ __forceinline__ void load_group(const u32x4 *__restrict__ W, int64_t g, float (&w)[kGroup]) {
-    const u32x4 a = __builtin_nontemporal_load(W + 2 * g);
-    const u32x4 b = __builtin_nontemporal_load(W + 2 * g + 1);
+// The 16 bf16 weights of a group (two 16-byte words) as exact fp32 values.
+__device__ __forceinline__ void unpack_group(const u32x4 a, const u32x4 b, float (&w)[kGroup]) {
     const uint32_t d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
         w[2 * k] = __uint_as_float(d[k] << 16);
         w[2 * k + 1] = __uint_as_float(d[k] & 0xFFFF0000u);
     }
+}
+
+__device__ __forceinline__ void load_group(const u32x4 *__restrict__ W, int64_t g, float (&w)[kGroup]) {
+    unpack_group(__builtin_nontemporal_load(W + 2 * g), __builtin_nontemporal_load(W + 2 * g + 1), w);
 }
 
 // ---------------------------------------------------------------------------

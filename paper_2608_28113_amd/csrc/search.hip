@@ -304,11 +304,23 @@ struct SearchArgs {
     float *err_init;
 };
 
+// Pointer `byte_off` bytes past `base`, with a 32-bit offset: the loads and
+// stores then take the uniform base from scalar registers and one 32-bit
+// offset per lane, instead of 64-bit address arithmetic per lane.
+template <typename T>
+__device__ __forceinline__ T *at_byte(T *base, uint32_t byte_off) {
+    using B = typename std::conditional<std::is_const<T>::value, const char, char>::type;
+    return reinterpret_cast<T *>(reinterpret_cast<B *>(base) + byte_off);
+}
+
 // One group per lane over the flat index g = r * Gc + i of the block, so the
 // lanes of a wave cover consecutive groups of a row (contiguous loads and
 // stores) and a lane's h slice is h[16 i .. 16 i + 15].  A launch normally
 // covers every group once; larger problems loop with a grid stride.
-template <int kInit, bool kStats>
+// kFlat: every array is contiguous (row strides equal the row widths) and
+// W's byte span fits in 32 bits, so group g sits at byte 32 g of W, 8 g of
+// the packed codes and g of the scale codes.
+template <int kInit, bool kStats, bool kFlat>
 __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs a) {
     __shared__ ScaleEntry tab[kTabSize];
     __shared__ ScaleEntry uniq[kMaxCode + 1];
@@ -330,28 +342,39 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
 
     for (;;) {
         float w[kGroup];
-        const u32x4 *src = a.W + (uint64_t)r * a.ldw_vec + 2 * (uint64_t)i;
-        load_group(src, 0, w);
+        if (kFlat) {
+            const u32x4 *src = at_byte(a.W, g << 5);
+            unpack_group(__builtin_nontemporal_load(src), __builtin_nontemporal_load(src + 1), w);
+        } else {
+            load_group(a.W + (uint64_t)r * a.ldw_vec + 2 * (uint64_t)i, 0, w);
+        }
         float hh[kGroup];
+        const float4 *hsrc = kFlat ? at_byte(a.h, i << 6) : a.h + 4 * (uint64_t)i;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float4 v = a.h[4 * (uint64_t)i + q];
+            const float4 v = hsrc[q];
             hh[4 * q] = v.x;
             hh[4 * q + 1] = v.y;
             hh[4 * q + 2] = v.z;
             hh[4 * q + 3] = v.w;
         }
-        const int given = kInit == kInitGiven ? (int)a.init[(uint64_t)r * a.ldi + i] : 0;
+        int given = 0;
+        if (kInit == kInitGiven) given = kFlat ? (int)*at_byte(a.init, g) : (int)a.init[(uint64_t)r * a.ldi + i];
         int code, shift;
         uint2 best_p;
         float e_best, e_init;
         search_group<kInit, kStats>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p, shift, e_best, e_init);
-        a.codes[(uint64_t)r * a.ldc + i] = (uint8_t)code;
-        a.packed[(uint64_t)r * a.ldp_vec + i] = best_p;
+        if (kFlat) {
+            *at_byte(a.codes, g) = (uint8_t)code;
+            *at_byte(a.packed, g << 3) = best_p;
+        } else {
+            a.codes[(uint64_t)r * a.ldc + i] = (uint8_t)code;
+            a.packed[(uint64_t)r * a.ldp_vec + i] = best_p;
+        }
         if (kStats) {
-            a.shift[g] = (int8_t)shift;
-            a.err_best[g] = e_best;
-            a.err_init[g] = e_init;
+            *at_byte(a.shift, g) = (int8_t)shift;
+            *at_byte(a.err_best, g << 2) = e_best;
+            *at_byte(a.err_init, g << 2) = e_init;
         }
 
         if (a.num_groups - g <= stride) break;
@@ -378,6 +401,31 @@ __global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *_
         load_group(W, g, w);
         const int c = min(max((int)codes[g], 1), kMaxCode);
         packed[g] = quantize_group(w, tab[c + kTabPad].R, make_uint2(0u, 0u));
+    }
+}
+
+template <bool kFlat>
+void launch_search(int init_mode, bool stats, dim3 grid, dim3 block, hipStream_t stream, const SearchArgs &a) {
+    if (!stats) {
+        switch (init_mode) {
+            case kInitMaxAbs:
+                hipLaunchKernelGGL((search_kernel<kInitMaxAbs, false, kFlat>), grid, block, 0, stream, a);
+                break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, false, kFlat>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, false, kFlat>), grid, block, 0, stream, a); break;
+        }
+    } else {
+        switch (init_mode) {
+            case kInitMaxAbs:
+                hipLaunchKernelGGL((search_kernel<kInitMaxAbs, true, kFlat>), grid, block, 0, stream, a);
+                break;
+            case kInitFourOverSix:
+                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, true, kFlat>), grid, block, 0, stream, a);
+                break;
+            default: hipLaunchKernelGGL((search_kernel<kInitGiven, true, kFlat>), grid, block, 0, stream, a); break;
+        }
     }
 }
 
@@ -447,24 +495,16 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
     a.shift = shift;
     a.err_best = err_best;
     a.err_init = err_init;
-    const dim3 grid(grid_for(out * Gc, kSearchThreads)), block(kSearchThreads);
-    if (!stats) {
-        switch (init_mode) {
-            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, false>), grid, block, 0, stream, a); break;
-            case kInitFourOverSix:
-                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, false>), grid, block, 0, stream, a);
-                break;
-            default: hipLaunchKernelGGL((search_kernel<kInitGiven, false>), grid, block, 0, stream, a); break;
-        }
-    } else {
-        switch (init_mode) {
-            case kInitMaxAbs: hipLaunchKernelGGL((search_kernel<kInitMaxAbs, true>), grid, block, 0, stream, a); break;
-            case kInitFourOverSix:
-                hipLaunchKernelGGL((search_kernel<kInitFourOverSix, true>), grid, block, 0, stream, a);
-                break;
-            default: hipLaunchKernelGGL((search_kernel<kInitGiven, true>), grid, block, 0, stream, a); break;
-        }
-    }
+    // The flat form needs contiguous arrays and 32-bit byte offsets: W spans
+    // 32 bytes per group (the largest array) and h 4 bytes per column.
+    const int64_t groups = out * Gc;
+    const bool flat = ldw == cols && ldc == Gc && ldp == cols / 2 && (init_mode != kInitGiven || ldi == Gc) &&
+                      groups <= ((int64_t)1 << 27) && cols <= ((int64_t)1 << 28);
+    const dim3 grid(grid_for(groups, kSearchThreads)), block(kSearchThreads);
+    if (flat)
+        launch_search<true>(init_mode, stats, grid, block, stream, a);
+    else
+        launch_search<false>(init_mode, stats, grid, block, stream, a);
     return launch_status();
 }
 
