@@ -22,10 +22,21 @@ def _check(status: int, where: str) -> None:
         raise HScaleError(status, where)
 
 
-def _stream(stream) -> int:
+def _stream(stream, device) -> int:
+    """Handle of `stream`, or of `device`'s current stream when None.  A
+    torch stream must belong to `device`, the device the operands are on."""
     if stream is None:
-        stream = torch.cuda.current_stream()
+        stream = torch.cuda.current_stream(device)
+    elif isinstance(stream, torch.cuda.Stream) and stream.device != device:
+        raise ValueError(f"stream is on {stream.device}, the operands on {device}")
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _call(device, fn, *args) -> int:
+    """Calls the library with `device` current, so that its launches go to
+    the device that holds the operands."""
+    with torch.cuda.device(device):
+        return fn(*args)
 
 
 def _on_device(t) -> bool:
@@ -107,10 +118,11 @@ def hdiag(X: torch.Tensor, h: torch.Tensor | None = None, workspace: torch.Tenso
     """h = diag(X^T X) (Sec. 3.2, Eq. 4) of bf16 X [tokens, in] as fp32 [in]."""
     _bf16_matrix(X, "X")
     T, n = X.shape
-    h = _out(h, "h", torch.float32, (n,), X.device)
-    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), X.device)
-    _check(_lib.hscale_hdiag(X.data_ptr(), T, n, h.data_ptr(), ws_ptr, ws_bytes, _stream(stream)),
-           "hscale_hdiag")
+    dev = X.device
+    h = _out(h, "h", torch.float32, (n,), dev)
+    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), dev)
+    _check(_call(dev, _lib.hscale_hdiag, X.data_ptr(), T, n, h.data_ptr(), ws_ptr, ws_bytes,
+                 _stream(stream, dev)), "hscale_hdiag")
     return h
 
 
@@ -133,18 +145,18 @@ def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | 
     mode, init_t = _init_mode(init, (m, n // 16), dev)
     scale_codes = _out(scale_codes, "scale_codes", torch.uint8, (m, n // 16), dev)
     packed_e2m1 = _out(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), dev)
-    s = _stream(stream)
+    s = _stream(stream, dev)
     if mode == _lib.HSCALE_INIT_MAXABS:
-        st = _lib.hscale_search_du(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
-                                   scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        st = _call(dev, _lib.hscale_search_du, W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
+                   scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_du")
     elif mode == _lib.HSCALE_INIT_4OVER6:
-        st = _lib.hscale_search_4over6(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
-                                       scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        st = _call(dev, _lib.hscale_search_4over6, W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
+                   scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_4over6")
     else:
-        st = _lib.hscale_search_from(W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
-                                     init_t.data_ptr(), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
+        st = _call(dev, _lib.hscale_search_from, W.data_ptr(), m, n, h.data_ptr(), down, up, float(global_scale),
+                   init_t.data_ptr(), scale_codes.data_ptr(), packed_e2m1.data_ptr(), s)
         _check(st, "hscale_search_from")
     return scale_codes, packed_e2m1
 
@@ -169,9 +181,9 @@ def search_block(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: in
     else:
         mode, _ = _init_mode(init, None, dev)
         iptr, ldi = 0, 0
-    st = _lib.hscale_search_block(W.data_ptr(), ldw, m, cols, h.data_ptr(), int(down), int(up),
-                                  float(global_scale), mode, iptr, ldi, scale_codes.data_ptr(), ldc,
-                                  packed_e2m1.data_ptr(), ldp, _stream(stream))
+    st = _call(dev, _lib.hscale_search_block, W.data_ptr(), ldw, m, cols, h.data_ptr(), int(down), int(up),
+               float(global_scale), mode, iptr, ldi, scale_codes.data_ptr(), ldc, packed_e2m1.data_ptr(), ldp,
+               _stream(stream, dev))
     _check(st, "hscale_search_block")
     return scale_codes, packed_e2m1
 
@@ -181,10 +193,11 @@ def hdiag_accumulate(X: torch.Tensor, h64: torch.Tensor, workspace: torch.Tensor
     """h64 += diag(X^T X) for one calibration batch (fp64 accumulator)."""
     _bf16_matrix(X, "X")
     T, n = X.shape
-    _tensor(h64, "h64", torch.float64, (n,), X.device)
-    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), X.device)
-    _check(_lib.hscale_hdiag_accumulate(X.data_ptr(), T, n, h64.data_ptr(), ws_ptr, ws_bytes,
-                                        _stream(stream)), "hscale_hdiag_accumulate")
+    dev = X.device
+    _tensor(h64, "h64", torch.float64, (n,), dev)
+    ws_ptr, ws_bytes = _workspace(workspace, hdiag_workspace_bytes(T, n), dev)
+    _check(_call(dev, _lib.hscale_hdiag_accumulate, X.data_ptr(), T, n, h64.data_ptr(), ws_ptr, ws_bytes,
+                 _stream(stream, dev)), "hscale_hdiag_accumulate")
     return h64
 
 
@@ -193,9 +206,11 @@ def hdiag_finalize(h64: torch.Tensor, h: torch.Tensor | None = None, stream=None
     if not _on_device(h64) or h64.dim() != 1:
         raise ValueError("h64 must be a 1-D fp64 CUDA tensor")
     n = h64.shape[0]
-    _tensor(h64, "h64", torch.float64, (n,), h64.device)
-    h = _out(h, "h", torch.float32, (n,), h64.device)
-    _check(_lib.hscale_hdiag_finalize(h64.data_ptr(), n, h.data_ptr(), _stream(stream)), "hscale_hdiag_finalize")
+    dev = h64.device
+    _tensor(h64, "h64", torch.float64, (n,), dev)
+    h = _out(h, "h", torch.float32, (n,), dev)
+    _check(_call(dev, _lib.hscale_hdiag_finalize, h64.data_ptr(), n, h.data_ptr(),
+                 _stream(stream, dev)), "hscale_hdiag_finalize")
     return h
 
 
@@ -204,10 +219,11 @@ def quantize(W: torch.Tensor, global_scale: float, scale_codes: torch.Tensor,
     """Packed E2M1 codes of W at the given scale codes (final re-quantization)."""
     _bf16_matrix(W, "W")
     m, n = W.shape
-    _tensor(scale_codes, "scale_codes", torch.uint8, (m, n // 16), W.device)
-    packed_e2m1 = _out(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), W.device)
-    _check(_lib.hscale_quantize(W.data_ptr(), m, n, float(global_scale), scale_codes.data_ptr(),
-                                packed_e2m1.data_ptr(), _stream(stream)), "hscale_quantize")
+    dev = W.device
+    _tensor(scale_codes, "scale_codes", torch.uint8, (m, n // 16), dev)
+    packed_e2m1 = _out(packed_e2m1, "packed_e2m1", torch.uint8, (m, n // 2), dev)
+    _check(_call(dev, _lib.hscale_quantize, W.data_ptr(), m, n, float(global_scale), scale_codes.data_ptr(),
+                 packed_e2m1.data_ptr(), _stream(stream, dev)), "hscale_quantize")
     return packed_e2m1
 
 
@@ -228,10 +244,10 @@ def search_stats(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: in
                shift=torch.empty(G, dtype=torch.int8, device=dev),
                err_best=torch.empty(G, dtype=torch.float32, device=dev),
                err_init=torch.empty(G, dtype=torch.float32, device=dev))
-    st = _lib.hscale_search_stats(W.data_ptr(), m, n, h.data_ptr(), int(down), int(up), float(global_scale), mode,
-                                  init_t.data_ptr() if init_t is not None else 0, out["scale_codes"].data_ptr(),
-                                  out["packed_e2m1"].data_ptr(), out["shift"].data_ptr(),
-                                  out["err_best"].data_ptr(), out["err_init"].data_ptr(), _stream(stream))
+    st = _call(dev, _lib.hscale_search_stats, W.data_ptr(), m, n, h.data_ptr(), int(down), int(up),
+               float(global_scale), mode, init_t.data_ptr() if init_t is not None else 0,
+               out["scale_codes"].data_ptr(), out["packed_e2m1"].data_ptr(), out["shift"].data_ptr(),
+               out["err_best"].data_ptr(), out["err_init"].data_ptr(), _stream(stream, dev))
     _check(st, "hscale_search_stats")
     return out
 
@@ -258,10 +274,9 @@ def shift_summary(shift: torch.Tensor, err_best: torch.Tensor, err_init: torch.T
                sum_rel=torch.empty(K, dtype=torch.float64, device=dev))
     need = _lib.hscale_shift_summary_workspace_bytes(groups, int(down), int(up))
     ws = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
-    st = _lib.hscale_shift_summary(shift.data_ptr(), err_best.data_ptr(), err_init.data_ptr(), groups, int(down),
-                                   int(up), out["count"].data_ptr(), out["sum_init"].data_ptr(),
-                                   out["sum_best"].data_ptr(), out["sum_rel"].data_ptr(), ws.data_ptr(), need,
-                                   _stream(stream))
+    st = _call(dev, _lib.hscale_shift_summary, shift.data_ptr(), err_best.data_ptr(), err_init.data_ptr(), groups,
+               int(down), int(up), out["count"].data_ptr(), out["sum_init"].data_ptr(), out["sum_best"].data_ptr(),
+               out["sum_rel"].data_ptr(), ws.data_ptr(), need, _stream(stream, dev))
     _check(st, "hscale_shift_summary")
     return out
 
@@ -291,7 +306,7 @@ def output_error(X: torch.Tensor, W: torch.Tensor, global_scale: float, scale_co
         row_err = torch.zeros(m, dtype=torch.float64, device=dev)
     _tensor(row_err, "row_err", torch.float64, (m,), dev)
     ws_ptr, ws_bytes = _workspace(workspace, output_error_workspace_bytes(T, n, m), dev)
-    _check(_lib.hscale_output_error(X.data_ptr(), T, n, W.data_ptr(), m, float(global_scale),
-                                    scale_codes.data_ptr(), packed_e2m1.data_ptr(), row_err.data_ptr(), ws_ptr,
-                                    ws_bytes, _stream(stream)), "hscale_output_error")
+    _check(_call(dev, _lib.hscale_output_error, X.data_ptr(), T, n, W.data_ptr(), m, float(global_scale),
+                 scale_codes.data_ptr(), packed_e2m1.data_ptr(), row_err.data_ptr(), ws_ptr, ws_bytes,
+                 _stream(stream, dev)), "hscale_output_error")
     return row_err
