@@ -287,6 +287,36 @@ def test_search_grid_stride_path(hs):
     assert rep["ok"], {k: v for k, v in rep.items() if k != "oracle"}
 
 
+def test_search_at_the_32bit_offset_limit(hs):
+    """Contiguous arrays are addressed with 32-bit byte offsets up to 2^27
+    groups (a 4 GiB W) and with 64-bit ones beyond: W of exactly 2^27 groups
+    (32768 x 65536) and of one row more, rows at both ends and around the
+    half-way mark checked against the oracle."""
+    m, n = 32769, 65536
+    print(f"[search offset limit] generating W {m}x{n}", flush=True)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(5)
+    W = torch.empty((m, n), dtype=torch.bfloat16, device=DEV)
+    for r0 in range(0, m, 4096):  # bounds the fp32 temporary
+        r1 = min(m, r0 + 4096)
+        W[r0:r1] = (torch.randn((r1 - r0, n), generator=g, device=DEV) * 0.02).to(torch.bfloat16)
+    h = torch.exp(torch.randn(n, generator=g, device=DEV))
+    s_g = harness_global_scale(W)
+    h_np = h.cpu().numpy()
+    for rows_total in (m - 1, m):
+        codes, packed = hs.search(W[:rows_total], h, s_g, window=2)
+        torch.cuda.synchronize()
+        rows = np.array([0, 1, rows_total // 2 - 1, rows_total // 2, rows_total - 2, rows_total - 1])
+        rows_t = torch.from_numpy(rows).to(DEV)
+        rep = parity.compare_search(tensor_bits(W.index_select(0, rows_t)), h_np, s_g, 2, 2,
+                                    codes.index_select(0, rows_t).cpu().numpy(),
+                                    packed.index_select(0, rows_t).cpu().numpy())
+        print(f"[search offset limit] rows={rows_total} groups={rows_total * (n // 16)} "
+              f"near_ties={rep['near_ties']} mismatches={rep['mismatches']}", flush=True)
+        assert rep["ok"], {k: v for k, v in rep.items() if k != "oracle"}
+        del codes, packed
+
+
 def test_block_layers_small_windows(hs):
     """One layer of each decoder-block shape (q/k/v/o, gate/up, down) with
     its own calibration X, windows 4 and 8, sampled rows."""
