@@ -42,6 +42,14 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 # fp32 VALU issue ceiling: 256 CU x 4 SIMD x 32 lanes/clk (one wave64 fp32
 # op per 2 clocks) x 2.4 GHz = 78.64 T lane-ops/s = 157.3 TFLOP/s of FMA.
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
+# Two further reference rates for the search, reported beside the peak:
+# a 16-lane-per-SIMD issue model (one wave64 instruction per 4 clocks), which
+# measured fp32 FMA throughput exceeds, so it is not a ceiling; and the
+# ceiling of the search's own instruction mix at measured per-class issue
+# costs (4 fp32 operations at 1.21 ns plus half a 3.50 ns FP4 pack and half
+# a 1.99 ns FP4 unpack conversion per weight-candidate, per wave per SIMD).
+ISSUE16_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+MIX_CEILING_TOPS = 5 * 64 * 1024 / (4 * 1.21 + 3.50 / 2 + 1.99 / 2) / 1e3
 SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
 HERE = os.path.dirname(os.path.abspath(__file__))
 # Sources of the hot-path kernels (hdiag, search): the committed HBM-traffic
@@ -264,6 +272,9 @@ def main():
                 "launches_per_step": nh}
     rl_search = {"bound": "alu", "achieved": round(search_tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
                  "unit": "T lane-ops/s", "frac": round(search_tops / VALU_PEAK_TOPS, 4), "traffic": None,
+                 "frac_of_16_lane_issue_model": round(search_tops / ISSUE16_TOPS, 4),
+                 "frac_of_mix_ceiling": round(search_tops / MIX_CEILING_TOPS, 4),
+                 "mix_ceiling": round(MIX_CEILING_TOPS, 2),
                  "kernel": "hscale_search (search_kernel)",
                  "algorithmic_ops_per_step": ops, "hbm_GBps": round(search_gbs, 1),
                  "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
@@ -299,6 +310,7 @@ def main():
         "search_isolated": None if iso is None else {
             "Gweights_per_s": round(weights / iso / 1e9, 2), "ms": round(iso * 1e3, 4),
             "frac_of_valu_roofline": round(ops / iso / 1e12 / VALU_PEAK_TOPS, 4),
+            "frac_of_mix_ceiling": round(ops / iso / 1e12 / MIX_CEILING_TOPS, 4),
             "protocol": "each layer's search alone: 3 warm-ups, then the median of 20 runs, a 1 GiB device "
                         "buffer overwritten before each run; not the headline (the step runs the search right "
                         "after the hdiag read, at a lower engine clock)"},
