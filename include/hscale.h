@@ -196,6 +196,43 @@ int hscale_search_from(const void *W, int64_t out, int64_t in,
                        hipStream_t stream);
 
 /*
+ * One layer of a batched search (hscale_search_layers).  Arrays contiguous
+ * and aligned as for hscale_search; init_codes is read only when init_mode
+ * is HSCALE_INIT_GIVEN (it may then equal scale_codes).
+ */
+typedef struct hscale_layer {
+    const void *W;             /* bf16 [out, in] */
+    int64_t out;
+    int64_t in;                /* in % 16 == 0 */
+    const float *h;            /* fp32 [in] */
+    float global_scale;        /* s_g of this layer */
+    const uint8_t *init_codes; /* uint8 [out, in / 16] or NULL */
+    uint8_t *scale_codes;      /* uint8 [out, in / 16], written */
+    uint8_t *packed_e2m1;      /* uint8 [out, in / 2], written */
+} hscale_layer;
+
+/*
+ * The search of several layers (for example the seven linear layers of a
+ * decoder block, each with its own W, h and s_g) in one launch per up to 32
+ * layers, with one shift set d = -down .. +up and one initial-code rule for
+ * all.  Each layer's result is bit for bit that of hscale_search_du /
+ * _4over6 / _from on it alone; batching only fills the GPU better when some
+ * layers are small and saves launches.
+ *
+ * layers     host array of `count` layers (count >= 0; NULL when 0).  It is
+ *            read during the call only.  Layers with out == 0 or in == 0 are
+ *            skipped.  Inputs may be shared between layers (one h for q, k
+ *            and v); no layer's outputs may overlap any buffer of another
+ *            layer (HSCALE_ERR_OVERLAP).
+ * init_mode  HSCALE_INIT_MAXABS, HSCALE_INIT_4OVER6 or HSCALE_INIT_GIVEN.
+ * Every layer is checked as hscale_search_du checks its arguments; the
+ * first failing layer's status is returned and nothing is launched.
+ */
+int hscale_search_layers(const hscale_layer *layers, int32_t count,
+                         int32_t down, int32_t up, int32_t init_mode,
+                         hipStream_t stream);
+
+/*
  * The general strided form, for a column block of a larger matrix (App. B,
  * the GPTQ combination searches W[:, i : i + B] with h[i : i + B] and the
  * layer's fixed s_g).  W points at the block's first element; group (r, k)

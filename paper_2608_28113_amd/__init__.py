@@ -11,5 +11,5 @@ The compute is in ``libhscale.so`` (hand-written HIP, C ABI in
 """
 from ._lib import HScaleError, EXPORTS  # noqa: F401
 from .ops import (hdiag, hdiag_accumulate, hdiag_finalize, hdiag_workspace_bytes, quantize,  # noqa: F401
-                  output_error, output_error_workspace_bytes, search, search_block, search_stats,
+                  output_error, output_error_workspace_bytes, search, search_block, search_layers, search_stats,
                   shift_summary)

@@ -29,6 +29,7 @@ EXPORTS = (
     "hscale_search_4over6",
     "hscale_search_from",
     "hscale_search_block",
+    "hscale_search_layers",
     "hscale_search_stats",
     "hscale_shift_summary_workspace_bytes",
     "hscale_shift_summary",
@@ -38,6 +39,13 @@ EXPORTS = (
 )
 
 HSCALE_INIT_MAXABS, HSCALE_INIT_4OVER6, HSCALE_INIT_GIVEN = 0, 1, 2
+
+
+class HScaleLayer(ctypes.Structure):
+    """struct hscale_layer of include/hscale.h (natural C layout)."""
+    _fields_ = [("W", ctypes.c_void_p), ("out", ctypes.c_int64), ("in_", ctypes.c_int64),
+                ("h", ctypes.c_void_p), ("global_scale", ctypes.c_float), ("init_codes", ctypes.c_void_p),
+                ("scale_codes", ctypes.c_void_p), ("packed_e2m1", ctypes.c_void_p)]
 
 _lib = None
 
@@ -80,6 +88,8 @@ def load() -> ctypes.CDLL:
     lib.hscale_search_from.restype = ctypes.c_int
     lib.hscale_search_block.argtypes = [P, i64, i64, i64, P, i32, i32, f32, i32, P, i64, P, i64, P, i64, P]
     lib.hscale_search_block.restype = ctypes.c_int
+    lib.hscale_search_layers.argtypes = [ctypes.POINTER(HScaleLayer), i32, i32, i32, i32, P]
+    lib.hscale_search_layers.restype = ctypes.c_int
     lib.hscale_search_stats.argtypes = [P, i64, i64, P, i32, i32, f32, i32, P, P, P, P, P, P, P]
     lib.hscale_search_stats.restype = ctypes.c_int
     lib.hscale_shift_summary_workspace_bytes.argtypes = [i64, i32, i32]
@@ -155,6 +165,15 @@ def hscale_search_block(W: int, ldw: int, out: int, cols: int, h: int, down: int
     return load().hscale_search_block(W or None, ldw, out, cols, h or None, down, up, global_scale,
                                       init_mode, init_codes or None, ldi, scale_codes or None, ldc,
                                       packed_e2m1 or None, ldp, stream or None)
+
+
+def hscale_search_layers(layers, down: int, up: int, init_mode: int, stream: int) -> int:
+    """layers: sequence of (W, out, in, h, global_scale, init_codes, scale_codes, packed_e2m1)
+    with device addresses as ints (0 for NULL)."""
+    arr = (HScaleLayer * max(len(layers), 1))()
+    for k, (W, out, in_, h, s_g, init, codes, packed) in enumerate(layers):
+        arr[k] = HScaleLayer(W or None, out, in_, h or None, s_g, init or None, codes or None, packed or None)
+    return load().hscale_search_layers(arr if layers else None, len(layers), down, up, init_mode, stream or None)
 
 
 def hscale_search_stats(W: int, out: int, in_: int, h: int, down: int, up: int, global_scale: float,

@@ -388,6 +388,82 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
     }
 }
 
+// Several independent layers searched by one launch, with the same shift
+// set and initial-code rule.  The layers' arrays are contiguous.  Each block
+// covers 256 consecutive groups of one layer and finds that layer among the
+// kernel arguments by its first block (a uniform scan over at most
+// kMaxBatchLayers entries), then proceeds as the single-layer search.
+constexpr int kMaxBatchLayers = 32;
+
+struct BatchLayer {
+    const u32x4 *W;
+    const float4 *h;
+    const uint8_t *init;
+    uint8_t *codes;
+    uint2 *packed;
+    uint32_t Gc;      // groups per row
+    uint32_t groups;  // rows * Gc
+    uint32_t block0;  // first block of the layer in the launch
+    float s_g;
+};
+
+struct BatchArgs {
+    BatchLayer layer[kMaxBatchLayers];
+    int count;
+    int down, up;
+};
+
+// kFlat: every layer's W spans less than 4 GiB, so 32-bit byte offsets from
+// the scalar bases address all of its arrays.
+template <int kInit, bool kFlat>
+__global__ __launch_bounds__(kSearchThreads) void search_layers_kernel(const BatchArgs a) {
+    int L = 0;
+#pragma unroll
+    for (int k = 1; k < kMaxBatchLayers; ++k)
+        if (k < a.count && blockIdx.x >= a.layer[k].block0) L = k;
+    const BatchLayer ly = a.layer[L];
+    __shared__ ScaleEntry tab[kTabSize];
+    __shared__ ScaleEntry uniq[kMaxCode + 1];
+    build_scale_table(tab, uniq, ly.s_g);
+
+    const uint32_t first = (blockIdx.x - ly.block0) * kSearchThreads;  // wave-uniform
+    const uint32_t g = first + threadIdx.x;
+    if (g >= ly.groups) return;
+    uint32_t i = first % ly.Gc + threadIdx.x;
+    while (i >= ly.Gc) i -= ly.Gc;
+
+    float w[kGroup];
+    if (kFlat) {
+        const u32x4 *src = at_byte(ly.W, g << 5);
+        unpack_group(__builtin_nontemporal_load(src), __builtin_nontemporal_load(src + 1), w);
+    } else {
+        load_group(ly.W, g, w);
+    }
+    float hh[kGroup];
+    const float4 *hsrc = kFlat ? at_byte(ly.h, i << 6) : ly.h + 4 * (uint64_t)i;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const float4 v = hsrc[q];
+        hh[4 * q] = v.x;
+        hh[4 * q + 1] = v.y;
+        hh[4 * q + 2] = v.z;
+        hh[4 * q + 3] = v.w;
+    }
+    int given = 0;
+    if (kInit == kInitGiven) given = kFlat ? (int)*at_byte(ly.init, g) : (int)ly.init[g];
+    int code, shift;
+    uint2 best_p;
+    float e_best, e_init;
+    search_group<kInit, false>(w, hh, tab, a.down, a.up, ly.s_g, given, code, best_p, shift, e_best, e_init);
+    if (kFlat) {
+        *at_byte(ly.codes, g) = (uint8_t)code;
+        *at_byte(ly.packed, g << 3) = best_p;
+    } else {
+        ly.codes[g] = (uint8_t)code;
+        ly.packed[g] = best_p;
+    }
+}
+
 __global__ __launch_bounds__(kSearchThreads) void quantize_kernel(const u32x4 *__restrict__ W,
                                                                   int64_t num_groups, float s_g,
                                                                   const uint8_t *__restrict__ codes,
@@ -429,10 +505,13 @@ void launch_search(int init_mode, bool stats, dim3 grid, dim3 block, hipStream_t
     }
 }
 
-int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
-                 float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, uint8_t *codes, int64_t ldc,
-                 uint8_t *packed, int64_t ldp, hipStream_t stream, int8_t *shift = nullptr,
-                 float *err_best = nullptr, float *err_init = nullptr) {
+// Host-side checks of a search over a block of `out` x `cols` weights inside
+// row-major arrays with the given row strides (statistics arrays optional):
+// HSCALE_OK when the arguments are valid, an empty problem included.
+int check_search(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
+                 float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, const uint8_t *codes,
+                 int64_t ldc, const uint8_t *packed, int64_t ldp, const int8_t *shift, const float *err_best,
+                 const float *err_init) {
     const bool stats = shift || err_best || err_init;
     if (out < 0 || cols < 0 || cols % kGroup != 0) return HSCALE_ERR_SHAPE;
     const int64_t Gc = cols / kGroup;
@@ -477,6 +556,18 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
             overlaps(err_best, groups * 4, err_init, groups * 4))
             return HSCALE_ERR_OVERLAP;
     }
+    return HSCALE_OK;
+}
+
+int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const float *h, int32_t down, int32_t up,
+                 float s_g, int32_t init_mode, const uint8_t *init_codes, int64_t ldi, uint8_t *codes, int64_t ldc,
+                 uint8_t *packed, int64_t ldp, hipStream_t stream, int8_t *shift = nullptr,
+                 float *err_best = nullptr, float *err_init = nullptr) {
+    const int status = check_search(W, ldw, out, cols, h, down, up, s_g, init_mode, init_codes, ldi, codes, ldc,
+                                    packed, ldp, shift, err_best, err_init);
+    if (status != HSCALE_OK || out == 0 || cols == 0) return status;
+    const bool stats = shift || err_best || err_init;
+    const int64_t Gc = cols / kGroup;
     SearchArgs a;
     a.W = static_cast<const u32x4 *>(W);
     a.ldw_vec = (uint64_t)ldw / 8;
@@ -506,6 +597,94 @@ int search_block(const void *W, int64_t ldw, int64_t out, int64_t cols, const fl
     else
         launch_search<false>(init_mode, stats, grid, block, stream, a);
     return launch_status();
+}
+
+// Launches one batch of at most kMaxBatchLayers non-empty, checked layers.
+template <int kInit>
+void launch_layers(const BatchArgs &a, uint32_t blocks, bool flat, hipStream_t stream) {
+    if (flat)
+        hipLaunchKernelGGL((search_layers_kernel<kInit, true>), dim3(blocks), dim3(kSearchThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((search_layers_kernel<kInit, false>), dim3(blocks), dim3(kSearchThreads), 0, stream, a);
+}
+
+int search_layers(const hscale_layer *layers, int32_t count, int32_t down, int32_t up, int32_t init_mode,
+                  hipStream_t stream) {
+    if (count < 0) return HSCALE_ERR_SHAPE;
+    if (init_mode < kInitMaxAbs || init_mode > kInitGiven) return HSCALE_ERR_SHAPE;
+    if (down < 0 || up < 0 || down > kMaxWindow || up > kMaxWindow) return HSCALE_ERR_WINDOW;
+    if (count == 0) return HSCALE_OK;
+    if (!layers) return HSCALE_ERR_NULL;
+    for (int32_t k = 0; k < count; ++k) {
+        const hscale_layer &l = layers[k];
+        const int status = check_search(l.W, l.in, l.out, l.in, l.h, down, up, l.global_scale, init_mode,
+                                        l.init_codes, l.in / kGroup, l.scale_codes, l.in / kGroup, l.packed_e2m1,
+                                        l.in / 2, nullptr, nullptr, nullptr);
+        if (status != HSCALE_OK) return status;
+    }
+    // The layers run concurrently: no layer's outputs may overlap another
+    // layer's inputs or outputs.
+    auto spans = [&](const hscale_layer &l, size_t &nw, size_t &nh, size_t &nc, size_t &np) {
+        const bool empty = l.out == 0 || l.in == 0;
+        nw = empty ? 0 : (size_t)l.out * (size_t)l.in * 2;
+        nh = empty ? 0 : (size_t)l.in * 4;
+        nc = empty ? 0 : (size_t)l.out * (size_t)(l.in / kGroup);
+        np = empty ? 0 : (size_t)l.out * (size_t)(l.in / 2);
+    };
+    for (int32_t x = 0; x < count; ++x) {
+        size_t xw, xh, xc, xp;
+        spans(layers[x], xw, xh, xc, xp);
+        for (int32_t y = 0; y < count; ++y) {
+            if (y == x) continue;
+            size_t yw, yh, yc, yp;
+            spans(layers[y], yw, yh, yc, yp);
+            const hscale_layer &a = layers[x], &b = layers[y];
+            const size_t yi = init_mode == kInitGiven ? yc : 0;
+            auto hits_b = [&](const void *p, size_t n) {
+                return overlaps(p, n, b.W, yw) || overlaps(p, n, b.h, yh) || overlaps(p, n, b.init_codes, yi) ||
+                       overlaps(p, n, b.scale_codes, yc) || overlaps(p, n, b.packed_e2m1, yp);
+            };
+            if (hits_b(a.scale_codes, xc) || hits_b(a.packed_e2m1, xp)) return HSCALE_ERR_OVERLAP;
+        }
+    }
+    BatchArgs a;
+    a.down = down;
+    a.up = up;
+    a.count = 0;
+    uint32_t blocks = 0;
+    bool flat = true, launched = false;
+    auto flush = [&]() {
+        if (a.count == 0) return;
+        launched = true;
+        switch (init_mode) {
+            case kInitMaxAbs: launch_layers<kInitMaxAbs>(a, blocks, flat, stream); break;
+            case kInitFourOverSix: launch_layers<kInitFourOverSix>(a, blocks, flat, stream); break;
+            default: launch_layers<kInitGiven>(a, blocks, flat, stream); break;
+        }
+        a.count = 0;
+        blocks = 0;
+        flat = true;
+    };
+    for (int32_t k = 0; k < count; ++k) {
+        const hscale_layer &l = layers[k];
+        if (l.out == 0 || l.in == 0) continue;
+        const int64_t groups = l.out * (l.in / kGroup);
+        BatchLayer &b = a.layer[a.count++];
+        b.W = static_cast<const u32x4 *>(l.W);
+        b.h = reinterpret_cast<const float4 *>(l.h);
+        b.init = l.init_codes;
+        b.codes = l.scale_codes;
+        b.packed = reinterpret_cast<uint2 *>(l.packed_e2m1);
+        b.Gc = (uint32_t)(l.in / kGroup);
+        b.groups = (uint32_t)groups;
+        b.block0 = blocks;
+        b.s_g = l.global_scale;
+        blocks += (uint32_t)((groups + kSearchThreads - 1) / kSearchThreads);
+        flat = flat && groups <= ((int64_t)1 << 27) && l.in <= ((int64_t)1 << 28);
+        if (a.count == kMaxBatchLayers) flush();
+    }
+    flush();
+    return launched ? launch_status() : HSCALE_OK;
 }
 
 }  // namespace
@@ -549,6 +728,11 @@ int hscale_search_stats(const void *W, int64_t out, int64_t in, const float *h, 
     if (out > 0 && in > 0 && (!shift || !err_best || !err_init)) return HSCALE_ERR_NULL;
     return search_block(W, in, out, in, h, down, up, global_scale, init_mode, init_codes, in / kGroup, scale_codes,
                         in / kGroup, packed_e2m1, in / 2, stream, shift, err_best, err_init);
+}
+
+int hscale_search_layers(const hscale_layer *layers, int32_t count, int32_t down, int32_t up, int32_t init_mode,
+                         hipStream_t stream) {
+    return search_layers(layers, count, down, up, init_mode, stream);
 }
 
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale, const uint8_t *scale_codes,

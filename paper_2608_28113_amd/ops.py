@@ -161,6 +161,55 @@ def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | 
     return scale_codes, packed_e2m1
 
 
+def search_layers(layers, window: int | None = None, down: int | None = None, up: int | None = None,
+                  init="maxabs", outputs=None, stream=None):
+    """The search of several layers in one launch (per up to 32 layers):
+    ``layers`` is a sequence of (W, h, global_scale), all on one device;
+    ``init`` is "maxabs", "4over6" or a sequence of per-layer uint8 code
+    tensors; ``outputs`` optionally a sequence of (scale_codes, packed_e2m1)
+    to write.  Returns the list of (scale_codes, packed_e2m1), each equal to
+    what ``search`` returns for that layer alone."""
+    layers = list(layers)
+    down, up = _window(window, down, up)
+    if outputs is not None:
+        outputs = list(outputs)
+        if len(outputs) != len(layers):
+            raise ValueError("give one (scale_codes, packed_e2m1) pair per layer")
+    given = None
+    if isinstance(init, str):
+        mode, _ = _init_mode(init, None, None)
+    else:
+        given = list(init)
+        if len(given) != len(layers):
+            raise ValueError("give one initial-code tensor per layer")
+        mode = _lib.HSCALE_INIT_GIVEN
+    dev = None
+    args, result = [], []
+    for k, layer in enumerate(layers):
+        if len(layer) != 3:
+            raise ValueError("each layer is (W, h, global_scale)")
+        W, h, s_g = layer
+        _bf16_matrix(W, f"W of layer {k}")
+        if dev is None:
+            dev = W.device
+        elif W.device != dev:
+            raise ValueError("all layers must be on one device")
+        m, n = W.shape
+        _tensor(h, f"h of layer {k}", torch.float32, (n,), dev)
+        codes, packed = (None, None) if outputs is None else outputs[k]
+        codes = _out(codes, f"scale_codes of layer {k}", torch.uint8, (m, n // 16), dev)
+        packed = _out(packed, f"packed_e2m1 of layer {k}", torch.uint8, (m, n // 2), dev)
+        iptr = 0
+        if given is not None:
+            iptr = _tensor(given[k], f"initial codes of layer {k}", torch.uint8, (m, n // 16), dev).data_ptr()
+        args.append((W.data_ptr(), m, n, h.data_ptr(), float(s_g), iptr, codes.data_ptr(), packed.data_ptr()))
+        result.append((codes, packed))
+    if not layers:
+        return result
+    _check(_call(dev, _lib.hscale_search_layers, args, down, up, mode, _stream(stream, dev)), "hscale_search_layers")
+    return result
+
+
 def search_block(W: torch.Tensor, h: torch.Tensor, global_scale: float, down: int, up: int,
                  scale_codes: torch.Tensor, packed_e2m1: torch.Tensor, init="maxabs", stream=None):
     """The search on a column block given as strided views: W = Wfull[:, a:b]

@@ -89,6 +89,24 @@ int main() {
     bad |= hscale_shift_summary((int8_t *)A, (float *)(A + 4096), (float *)(A + 8192), 1000, 9, 6,
                                 (uint64_t *)(A + 12288), (double *)(A + 12296), (double *)(A + 16384),
                                 (double *)(A + 20480), A + 24576, 1 << 20, nullptr) != HSCALE_ERR_OVERLAP;
+    {
+        hscale_layer L[3] = {};
+        for (int k = 0; k < 3; ++k) {
+            char *b = A + (k + 1) * (1 << 16);
+            L[k] = hscale_layer{b, 4, 64, (const float *)(b + 4096), 1e-3f, nullptr, (uint8_t *)(b + 8192),
+                                (uint8_t *)(b + 12288)};
+        }
+        bad |= hscale_search_layers(nullptr, 0, 4, 4, 0, nullptr) != HSCALE_OK;
+        bad |= hscale_search_layers(L, 3, 126, 4, 0, nullptr) != HSCALE_ERR_WINDOW;
+        bad |= hscale_search_layers(L, 3, 4, 4, 2, nullptr) != HSCALE_ERR_NULL;
+        hscale_layer over[2] = {L[0], L[1]};
+        over[1].scale_codes = (uint8_t *)L[0].W;
+        bad |= hscale_search_layers(over, 2, 4, 4, 0, nullptr) != HSCALE_ERR_OVERLAP;
+        hscale_layer empty[2] = {L[0], L[1]};
+        empty[0].out = 0;
+        empty[1].in = 0;
+        bad |= hscale_search_layers(empty, 2, 4, 4, 0, nullptr) != HSCALE_OK;
+    }
     for (int s = -9; s <= 1; ++s) bad |= hscale_status_string(s) == nullptr;
     std::printf(bad ? "sanitize driver: FAILED\n" : "sanitize driver: ok\n");
     return bad;

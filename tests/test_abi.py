@@ -268,3 +268,42 @@ def test_torch_front_end_rejects_bad_tensors_diagnostics():
     with pytest.raises(ValueError):
         ops.output_error(torch.zeros(8, 16, dtype=torch.bfloat16), W, 1e-3, torch.zeros(4, 1, dtype=torch.uint8),
                          torch.zeros(4, 8, dtype=torch.uint8))
+
+
+def test_search_layers_validation(L):
+    """The batched search checks every layer as hscale_search_du does, and
+    refuses outputs that overlap another layer's buffers, before any launch."""
+    m, n = 4, 64
+    B = 1 << 24  # layer k's buffers start at (k + 1) * B
+
+    def layer(k, **kw):
+        base = (k + 1) * B
+        d = dict(W=base, out=m, in_=n, h=base + A, s=1e-3, init=0, codes=base + 2 * A, packed=base + 3 * A)
+        d.update(kw)
+        return (d["W"], d["out"], d["in_"], d["h"], d["s"], d["init"], d["codes"], d["packed"])
+
+    def call(layers, down=4, up=4, mode=0):
+        return L.hscale_search_layers(layers, down, up, mode, 0)
+
+    good = [layer(0), layer(1), layer(2)]
+    assert call([]) == 0                                   # nothing to do
+    assert call([layer(0, out=0), layer(1, in_=0)]) == 0   # every layer empty: no launch
+    assert L.load().hscale_search_layers(None, -1, 4, 4, 0, None) == -2
+    assert L.load().hscale_search_layers(None, 2, 4, 4, 0, None) == -1
+    assert call(good, down=-1) == -4
+    assert call(good, up=126) == -4
+    assert call(good, mode=3) == -2
+    assert call(good[:1] + [layer(1, in_=65)]) == -2
+    assert call(good[:2] + [layer(2, s=0.0)]) == -5
+    assert call([layer(0, W=0)] + good[1:]) == -1
+    assert call(good, mode=2) == -1                        # given codes but no init pointer
+    assert call([layer(0, W=B + 8)]) == -3
+    assert call([layer(0, packed=B + 3 * A + 4)]) == -3
+    # within a layer: codes over its own W
+    assert call([layer(0, codes=B + 16)]) == -8
+    # across layers: layer 1's codes over layer 0's W, h or packed codes
+    assert call([layer(0), layer(1, codes=B)]) == -8
+    assert call([layer(0), layer(1, packed=B + A)]) == -8
+    assert call([layer(0), layer(1, codes=B + 3 * A + 8)]) == -8
+    # layer 0's codes as layer 1's initial codes (read while layer 0 writes them)
+    assert call([layer(0, init=B + 5 * A), layer(1, init=B + 2 * A)], mode=2) == -8

@@ -171,3 +171,57 @@ def test_host_tensors_refused_without_stubs():
     with pytest.raises(ValueError):
         ops.search_block(W, torch.zeros(n), 1e-3, 4, 4, torch.zeros(m, n // 16, dtype=torch.uint8),
                          torch.zeros(m, n // 2, dtype=torch.uint8), stream=0)
+
+
+def _layers():
+    return [(bf(m, n), f32(n), 1e-3), (bf(2 * m, n), f32(n), 2e-3), (bf(m, 2 * n), f32(2 * n), 1e-3)]
+
+
+def test_search_layers_good_call_reaches_the_library(fake_gpu):
+    with pytest.raises(Reached):
+        ops.search_layers(_layers(), window=4, stream=0)
+    with pytest.raises(Reached):
+        ops.search_layers(_layers(), down=9, up=6, init="4over6", stream=0)
+    L = _layers()
+    with pytest.raises(Reached):
+        ops.search_layers(L, window=4, init=[u8(W.shape[0], W.shape[1] // 16) for W, _, _ in L],
+                          outputs=[(u8(W.shape[0], W.shape[1] // 16), u8(W.shape[0], W.shape[1] // 2))
+                                   for W, _, _ in L], stream=0)
+    assert ops.search_layers([], window=4, stream=0) == []
+
+
+@pytest.mark.parametrize("k", [0, 2])
+@pytest.mark.parametrize("part", ["W", "h", "codes", "packed", "init"])
+@pytest.mark.parametrize("mutation", ["on_host", "wrong_dtype", "strided"])
+def test_search_layers_bad_buffer_refused(fake_gpu, k, part, mutation):
+    L = _layers()
+    mut = globals()[mutation]
+    outs = [(u8(W.shape[0], W.shape[1] // 16), u8(W.shape[0], W.shape[1] // 2)) for W, _, _ in L]
+    init = [u8(W.shape[0], W.shape[1] // 16) for W, _, _ in L]
+    W, h, s = L[k]
+    if part == "W":
+        L[k] = (mut(W), h, s)
+    elif part == "h":
+        L[k] = (W, mut(h), s)
+    elif part == "codes":
+        outs[k] = (mut(outs[k][0]), outs[k][1])
+    elif part == "packed":
+        outs[k] = (outs[k][0], mut(outs[k][1]))
+    else:
+        init[k] = mut(init[k])
+    with pytest.raises(ValueError):
+        ops.search_layers(L, window=4, init=init, outputs=outs, stream=0)
+
+
+def test_search_layers_shape_mismatches_refused(fake_gpu):
+    L = _layers()
+    with pytest.raises(ValueError):
+        ops.search_layers(L, window=4, outputs=[(u8(m, n // 16), u8(m, n // 2))], stream=0)  # too few
+    with pytest.raises(ValueError):
+        ops.search_layers(L, window=4, init=[u8(m, n // 16)], stream=0)
+    with pytest.raises(ValueError):
+        ops.search_layers([(bf(m, n), f32(n))], window=4, stream=0)                       # no s_g
+    with pytest.raises(ValueError):
+        ops.search_layers([(bf(m, n), f32(n + 16), 1e-3)], window=4, stream=0)            # h length
+    with pytest.raises(ValueError):
+        ops.search_layers(L, window=4, down=1, up=1, stream=0)
