@@ -107,12 +107,21 @@ def measured_traffic(workload: str):
     if prof.get("kernel_source_sha256_16") != source_hash(HOT_SOURCES):
         return None
     t = prof.get("traffic", {})
+    steps = prof.get("steps_profiled")
+
+    def per_step(name):
+        # mean bytes per dispatch x dispatches per step (several hdiag
+        # calls in a multi-layer step)
+        k = t[name]
+        n = k["dispatches"] / steps if steps and "dispatches" in k else 1.0
+        return (k["read_bytes"] + k["write_bytes"]) * n
 
     def tot(*names):
         if not all(n in t for n in names):
             return None
-        return sum(t[n]["read_bytes"] + t[n]["write_bytes"] for n in names)
-    return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot("search_kernel"),
+        return sum(per_step(n) for n in names)
+    search = "search_layers_kernel" if "search_layers_kernel" in t else "search_kernel"
+    return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot(search),
             "source": os.path.relpath(path, HERE)}
 
 
