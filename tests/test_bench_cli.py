@@ -1,9 +1,11 @@
-"""bench.py's command-line contract on the CPU: more than one GPU is refused
-with a message before anything touches a GPU, and inconsistent window flags
-are rejected."""
+"""bench.py on the CPU: its command-line contract (more than one GPU is
+refused with a message before anything touches a GPU, inconsistent window
+flags are rejected), and the committed profiles it quotes."""
 import subprocess
 import sys
 from pathlib import Path
+
+import pytest
 
 ROOT = Path(__file__).resolve().parent.parent
 
@@ -24,3 +26,27 @@ def test_window_flags_are_checked():
     assert r.returncode == 2 and "--down and --up" in r.stderr
     r = _run("--window", "4", "--down", "9", "--up", "6")
     assert r.returncode == 2
+
+
+@pytest.mark.parametrize("workload", ["down_proj", "attn_proj", "down_proj_70b", "block"])
+def test_committed_profile_traffic_matches_the_algorithmic_bytes(workload):
+    """The rocprofv3 summary under profiles/ that the bench line quotes as
+    `traffic` is per step and equals the algorithmic bytes of hdiag (X read
+    once) and of the search (W read, codes written) within 1%."""
+    import bench
+    from synth.workloads import CONFIGS, block_workloads
+
+    t = bench.measured_traffic(workload)
+    if t is None:
+        pytest.skip(f"profiles/{workload}.json is absent or older than the kernel sources")
+    if workload == "block":
+        wls = block_workloads()
+        # X_attn and X_mlp (262144 x 4096) and X_down (262144 x 14336)
+        hd = 2 * (2 * 262144 * 4096 + 4 * 4096) + (2 * 262144 * 14336 + 4 * 14336)
+        weights = sum(wl.out * wl.inp for wl in wls.values())
+    else:
+        wl = CONFIGS[workload]
+        hd = 2 * wl.tokens * wl.inp + 4 * wl.inp
+        weights = wl.out * wl.inp
+    assert abs(t["hdiag"] / hd - 1) < 0.01, (t["hdiag"], hd)
+    assert abs(t["search"] / (bench.SEARCH_BYTES_PER_WEIGHT * weights) - 1) < 0.01
