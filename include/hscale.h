@@ -25,8 +25,9 @@
  * Conventions shared by every entry point
  *   - All pointers are device pointers (hipMalloc'd or torch CUDA tensors)
  *     unless stated.  The caller allocates and owns every buffer; the library
- *     allocates nothing, keeps no global state, never synchronises and is
- *     safe to call from several host threads on different streams.
+ *     allocates nothing, never synchronises and is safe to call from several
+ *     host threads on different streams.  Its only global state is the
+ *     static scratch of hscale_hdiag_noalloc (see there).
  *   - Work is enqueued on `stream` (NULL = the default stream) and is
  *     complete only once the caller synchronises that stream.  Arguments are
  *     validated on the host before anything is enqueued; on any error
@@ -73,7 +74,10 @@ typedef enum hscale_status {
     HSCALE_ERR_SCALE = -5,     /* global_scale not finite, not > 0, or out of range */
     HSCALE_ERR_WORKSPACE = -6, /* workspace too small */
     HSCALE_ERR_HIP = -7,       /* the HIP runtime rejected a launch */
-    HSCALE_ERR_OVERLAP = -8    /* an output overlaps an input */
+    HSCALE_ERR_OVERLAP = -8,   /* an output overlaps an input */
+    HSCALE_ERR_SCRATCH = -9,   /* the problem needs more than the static scratch
+                                  of hscale_hdiag_noalloc holds */
+    HSCALE_ERR_DEVICE = -10    /* the stream is not on the current device */
 } hscale_status;
 
 /* How the search chooses each group's initial code c0 before the walk. */
@@ -118,6 +122,31 @@ size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in);
  */
 int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
                  void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * hscale_hdiag for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same h, bit for bit, with the slice partials held in a static device
+ * array of the library (8 MiB per GPU, kept until the process ends) instead
+ * of a caller workspace.  The call allocates nothing.
+ *
+ * X, tokens, in, h   as hscale_hdiag.
+ * stream             must belong to the current device (HSCALE_ERR_DEVICE
+ *                    otherwise); NULL is the current device's default stream.
+ *
+ * Limit: problems whose hscale_hdiag_workspace_bytes(tokens, in) exceeds
+ * 8 MiB are rejected with HSCALE_ERR_SCRATCH before anything is enqueued;
+ * every in <= 2^20 (any tokens) fits.  The first call on a device looks up
+ * that device's copy of the array (hipGetSymbolAddress) and keeps its
+ * address; a failed lookup returns HSCALE_ERR_HIP.
+ *
+ * All calls on one GPU share that GPU's array: calls that may run at the
+ * same time on one GPU (different streams, or host threads that do not
+ * order their streams) race on it and give undefined h.  Calls ordered on
+ * one stream are safe; nothing is carried from one call to the next.
+ */
+int hscale_hdiag_noalloc(const void *X, int64_t tokens, int64_t in, float *h,
+                         hipStream_t stream);
 
 /*
  * Streamed calibration (Eq. 4 over batches): h64[j] += sum_t X[t, j]^2 for

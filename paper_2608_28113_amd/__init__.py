@@ -10,6 +10,6 @@ The compute is in ``libhscale.so`` (hand-written HIP, C ABI in
 ``include/hscale.h``); this package is its thin Python binding.
 """
 from ._lib import HScaleError, EXPORTS  # noqa: F401
-from .ops import (hdiag, hdiag_accumulate, hdiag_finalize, hdiag_workspace_bytes, quantize,  # noqa: F401
+from .ops import (hdiag, hdiag_accumulate, hdiag_finalize, hdiag_noalloc, hdiag_workspace_bytes, quantize,  # noqa: F401
                   output_error, output_error_workspace_bytes, search, search_block, search_layers, search_stats,
                   shift_summary)

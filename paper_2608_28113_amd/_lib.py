@@ -14,7 +14,7 @@ HSCALE_OK = 0
 STATUS = {
     0: "HSCALE_OK", -1: "HSCALE_ERR_NULL", -2: "HSCALE_ERR_SHAPE", -3: "HSCALE_ERR_ALIGN",
     -4: "HSCALE_ERR_WINDOW", -5: "HSCALE_ERR_SCALE", -6: "HSCALE_ERR_WORKSPACE",
-    -7: "HSCALE_ERR_HIP", -8: "HSCALE_ERR_OVERLAP",
+    -7: "HSCALE_ERR_HIP", -8: "HSCALE_ERR_OVERLAP", -9: "HSCALE_ERR_SCRATCH", -10: "HSCALE_ERR_DEVICE",
 }
 
 # Every symbol include/hscale.h declares.
@@ -22,6 +22,7 @@ EXPORTS = (
     "hscale_status_string",
     "hscale_hdiag_workspace_bytes",
     "hscale_hdiag",
+    "hscale_hdiag_noalloc",
     "hscale_hdiag_accumulate",
     "hscale_hdiag_finalize",
     "hscale_search",
@@ -72,6 +73,8 @@ def load() -> ctypes.CDLL:
     lib.hscale_hdiag_workspace_bytes.restype = sz
     lib.hscale_hdiag.argtypes = [P, i64, i64, P, P, sz, P]
     lib.hscale_hdiag.restype = ctypes.c_int
+    lib.hscale_hdiag_noalloc.argtypes = [P, i64, i64, P, P]
+    lib.hscale_hdiag_noalloc.restype = ctypes.c_int
     lib.hscale_search.argtypes = [P, i64, i64, P, i32, f32, P, P, P]
     lib.hscale_search.restype = ctypes.c_int
     lib.hscale_search_du.argtypes = [P, i64, i64, P, i32, i32, f32, P, P, P]
@@ -116,6 +119,10 @@ def hscale_hdiag(X: int, tokens: int, in_: int, h: int, workspace: int, workspac
                  stream: int) -> int:
     return load().hscale_hdiag(X or None, tokens, in_, h or None, workspace or None,
                                workspace_bytes, stream or None)
+
+
+def hscale_hdiag_noalloc(X: int, tokens: int, in_: int, h: int, stream: int) -> int:
+    return load().hscale_hdiag_noalloc(X or None, tokens, in_, h or None, stream or None)
 
 
 def hscale_search(W: int, out: int, in_: int, h: int, window: int, global_scale: float,

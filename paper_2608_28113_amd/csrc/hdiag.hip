@@ -13,6 +13,14 @@
 
 #include "common.h"
 
+#include <mutex>
+
+// Device scratch of hscale_hdiag_noalloc (fp64 slice partials), sized for
+// the largest problem it accepts: every hdiag plan with in <= 2^20 columns
+// needs at most 8 MiB.
+constexpr size_t kHdiagScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kHdiagScratchBytes];
+
 namespace {
 
 constexpr int kHdThreads = 256;
@@ -134,8 +142,9 @@ __global__ __launch_bounds__(256) void hdiag_finalize_kernel(const double *__res
     if (j < in) h[j] = (float)h64[j];
 }
 
-int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, void *workspace,
-              size_t workspace_bytes, hipStream_t stream) {
+// Checks of X and the output that need no workspace and no HIP call: HSCALE_OK
+// when the arguments are valid (in == 0 included).
+int hdiag_check_io(const void *X, int64_t tokens, int64_t in, const float *h, const double *h64) {
     if (tokens < 0 || in < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
     if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
     if (in == 0) return HSCALE_OK;
@@ -143,19 +152,32 @@ int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, 
     if (!accumulate && !h) return HSCALE_ERR_NULL;
     if (!accumulate && !aligned(h, 4)) return HSCALE_ERR_ALIGN;
     if (accumulate && !aligned(h64, 8)) return HSCALE_ERR_ALIGN;
+    if (tokens > 0) {
+        if (!X) return HSCALE_ERR_NULL;
+        if (!aligned(X, 16)) return HSCALE_ERR_ALIGN;
+        const size_t nx = (size_t)tokens * (size_t)in * 2;
+        const size_t nout = accumulate ? (size_t)in * 8 : (size_t)in * 4;
+        const void *out = accumulate ? (const void *)h64 : (const void *)h;
+        if (overlaps(out, nout, X, nx)) return HSCALE_ERR_OVERLAP;
+    }
+    return HSCALE_OK;
+}
+
+int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, void *workspace,
+              size_t workspace_bytes, hipStream_t stream) {
+    const int status = hdiag_check_io(X, tokens, in, h, h64);
+    if (status != HSCALE_OK || in == 0) return status;
+    const bool accumulate = h64 != nullptr;
     const HdiagPlan p = hdiag_plan(tokens, in);
     const size_t need = hscale_hdiag_workspace_bytes(tokens, in);
     const size_t nout = accumulate ? (size_t)in * 8 : (size_t)in * 4;
     const void *out = accumulate ? (const void *)h64 : (const void *)h;
     if (tokens > 0) {
-        if (!X) return HSCALE_ERR_NULL;
-        if (!aligned(X, 16)) return HSCALE_ERR_ALIGN;
         if (workspace_bytes < need) return HSCALE_ERR_WORKSPACE;
         if (!workspace) return HSCALE_ERR_NULL;
         if (!aligned(workspace, 16)) return HSCALE_ERR_ALIGN;
         const size_t nx = (size_t)tokens * (size_t)in * 2;
-        if (overlaps(out, nout, X, nx) || overlaps(workspace, need, X, nx) || overlaps(workspace, need, out, nout))
-            return HSCALE_ERR_OVERLAP;
+        if (overlaps(workspace, need, X, nx) || overlaps(workspace, need, out, nout)) return HSCALE_ERR_OVERLAP;
         dim3 grid((unsigned)p.tiles, (unsigned)p.slices);
         hipLaunchKernelGGL(hdiag_partial, grid, dim3(kHdThreads), 0, stream, static_cast<const u32x4 *>(X),
                            tokens, in, p.slice_tokens, static_cast<double *>(workspace));
@@ -168,6 +190,43 @@ int hdiag_run(const void *X, int64_t tokens, int64_t in, float *h, double *h64, 
     else
         launch_tree<false>(static_cast<const double *>(workspace), p.slices, in, h, nullptr, stream);
     return launch_status();
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch for hscale_hdiag_noalloc: the slice partials live in a
+// device array of the library instead of a caller workspace.  Each GPU holds
+// its own copy at its own address, looked up once per device with that
+// device current; host code uses only the looked-up address (the array's
+// name is a host-side stand-in, not a device address).  The partials kernel
+// writes every partial the tree reads, so nothing needs clearing between
+// calls.
+// ---------------------------------------------------------------------------
+
+constexpr int kScratchDevices = 64;
+
+struct ScratchSlot {
+    std::once_flag once;
+    void *ptr = nullptr;
+    hipError_t err = hipSuccess;
+};
+
+ScratchSlot g_scratch_slot[kScratchDevices];
+
+// The scratch address on the device `stream` runs on, which must be the
+// current device (the lookup is made with it current).
+int scratch_address(hipStream_t stream, void **out) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur < 0 || cur >= kScratchDevices) return HSCALE_ERR_HIP;
+    if (stream) {
+        int dev = -1;
+        if (hipStreamGetDevice(stream, &dev) != hipSuccess) return HSCALE_ERR_HIP;
+        if (dev != cur) return HSCALE_ERR_DEVICE;
+    }
+    ScratchSlot &s = g_scratch_slot[cur];
+    std::call_once(s.once, [&s] { s.err = hipGetSymbolAddress(&s.ptr, HIP_SYMBOL(scratch)); });
+    if (s.err != hipSuccess || !s.ptr) return HSCALE_ERR_HIP;
+    *out = s.ptr;
+    return HSCALE_OK;
 }
 
 }  // namespace
@@ -185,6 +244,9 @@ const char *hscale_status_string(int status) {
         case HSCALE_ERR_WORKSPACE: return "HSCALE_ERR_WORKSPACE: workspace too small";
         case HSCALE_ERR_HIP: return "HSCALE_ERR_HIP: the HIP runtime rejected a launch";
         case HSCALE_ERR_OVERLAP: return "HSCALE_ERR_OVERLAP: an output overlaps an input";
+        case HSCALE_ERR_SCRATCH:
+            return "HSCALE_ERR_SCRATCH: the problem needs more scratch than the library's static buffer holds";
+        case HSCALE_ERR_DEVICE: return "HSCALE_ERR_DEVICE: the stream is not on the current device";
         default: return "unknown hscale status";
     }
 }
@@ -198,6 +260,20 @@ size_t hscale_hdiag_workspace_bytes(int64_t tokens, int64_t in) {
 int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h, void *workspace, size_t workspace_bytes,
                  hipStream_t stream) {
     return hdiag_run(X, tokens, in, h, nullptr, workspace, workspace_bytes, stream);
+}
+
+int hscale_hdiag_noalloc(const void *X, int64_t tokens, int64_t in, float *h, hipStream_t stream) {
+    // Every host-side check comes before the first HIP call.
+    const int status = hdiag_check_io(X, tokens, in, h, nullptr);
+    if (status != HSCALE_OK || in == 0) return status;
+    const size_t need = hscale_hdiag_workspace_bytes(tokens, in);
+    if (need > kHdiagScratchBytes) return HSCALE_ERR_SCRATCH;
+    void *ws = nullptr;
+    if (need > 0) {
+        const int st = scratch_address(stream, &ws);
+        if (st != HSCALE_OK) return st;
+    }
+    return hdiag_run(X, tokens, in, h, nullptr, ws, need, stream);
 }
 
 int hscale_hdiag_accumulate(const void *X, int64_t tokens, int64_t in, double *h64, void *workspace,

@@ -126,6 +126,19 @@ def hdiag(X: torch.Tensor, h: torch.Tensor | None = None, workspace: torch.Tenso
     return h
 
 
+def hdiag_noalloc(X: torch.Tensor, h: torch.Tensor, stream=None) -> torch.Tensor:
+    """hdiag into a caller-provided fp32 h [in] with the library's static
+    scratch instead of a workspace: the call allocates no device memory
+    (problems up to 2^20 columns; calls that may overlap on one GPU race)."""
+    _bf16_matrix(X, "X")
+    T, n = X.shape
+    dev = X.device
+    _tensor(h, "h", torch.float32, (n,), dev)
+    _check(_call(dev, _lib.hscale_hdiag_noalloc, X.data_ptr(), T, n, h.data_ptr(), _stream(stream, dev)),
+           "hscale_hdiag_noalloc")
+    return h
+
+
 def search(W: torch.Tensor, h: torch.Tensor, global_scale: float, window: int | None = None,
            down: int | None = None, up: int | None = None, init="maxabs",
            scale_codes: torch.Tensor | None = None, packed_e2m1: torch.Tensor | None = None, stream=None):

@@ -80,6 +80,30 @@ def test_hdiag_validation(L):
     assert L.hscale_hdiag(0, 64, 0, 0, 0, 0, 0) == 0
 
 
+def test_hdiag_noalloc_validation(L):
+    """The static-scratch entry point checks its arguments, and the scratch
+    limit, before its first HIP call (so these run without a GPU)."""
+    assert L.hscale_hdiag_noalloc(A, 64, 33, 2 * A, 0) == -2
+    assert L.hscale_hdiag_noalloc(A, -1, 32, 2 * A, 0) == -2
+    assert L.hscale_hdiag_noalloc(0, 64, 32, 2 * A, 0) == -1
+    assert L.hscale_hdiag_noalloc(A, 64, 32, 0, 0) == -1
+    assert L.hscale_hdiag_noalloc(A + 8, 64, 32, 2 * A, 0) == -3
+    assert L.hscale_hdiag_noalloc(A, 64, 32, 2 * A + 2, 0) == -3
+    assert L.hscale_hdiag_noalloc(A, 64, 32, A + 64, 0) == -8
+    assert L.hscale_hdiag_noalloc(0, 64, 0, 0, 0) == 0
+    # every plan with in <= 2^20 columns fits the 8 MiB scratch; wider
+    # problems are refused with HSCALE_ERR_SCRATCH
+    limit = 8 << 20
+    for n in (16, 512, 528, 14336, 28672, 917504, 917520, 1 << 20):
+        for T in (1, 256, 4096, 262144, 1 << 24):
+            assert L.hscale_hdiag_workspace_bytes(T, n) <= limit, (T, n)
+    n = (1 << 20) + 16
+    assert L.hscale_hdiag_workspace_bytes(1, n) > limit
+    assert L.hscale_hdiag_noalloc(A, 1, n, 1 << 40, 0) == -9
+    assert L.status_string(-9).startswith("HSCALE_ERR_SCRATCH")
+    assert L.status_string(-10).startswith("HSCALE_ERR_DEVICE")
+
+
 def test_search_validation(L):
     m, n = 4, 64
     W, h, codes, packed = A, 2 * A, 3 * A, 4 * A
