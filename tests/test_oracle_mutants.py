@@ -58,6 +58,9 @@ MUTANTS = {
     "output_error_overwrites": ("row_err[r] += y * y;", "row_err[r] = y * y;"),
     "summary_rel_wrong_denominator": ("sum_rel[k] += (e_init[g] - e_best[g]) / e_init[g];",
                                       "sum_rel[k] += (e_init[g] - e_best[g]) / e_best[g];"),
+    "summary_rel_unguarded_zero_init": ("if (e_init[g] > 0.0) sum_rel[k] +=", "if (1) sum_rel[k] +="),
+    "summary_rel_not_relative": ("sum_rel[k] += (e_init[g] - e_best[g]) / e_init[g];",
+                                 "sum_rel[k] += (e_init[g] - e_best[g]);"),
     "summary_swaps_sums": ("sum_init[k] += e_init[g];\n        sum_best[k] += e_best[g];",
                            "sum_init[k] += e_best[g];\n        sum_best[k] += e_init[g];"),
     "stats_init_error_at_wrong_shift": ("if (d == 0 && e_init) *e_init = e;", "if (d == 1 && e_init) *e_init = e;"),
