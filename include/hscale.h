@@ -51,7 +51,10 @@
  *   x_j = fp32(w_j * R[c]); code_j = E2M1 round-to-nearest-even of x_j
  *     (ties to the even index, |x| > 5 -> 6), sign copied from w_j
  *   score E(c) = sum_j h_j (w_j - v_j S[c])^2 evaluated in fp32; the first
- *     minimum in increasing d wins
+ *     minimum in increasing d wins.  A score that overflows fp32 is +Inf
+ *     and ties with every other +Inf score, so a group whose scores all
+ *     overflow (finite but huge h) takes the smallest shift d = -down; its
+ *     packed codes are still the quantization at the code it reports.
  */
 #ifndef HSCALE_H
 #define HSCALE_H
@@ -386,8 +389,11 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in,
  * the codes it chose.
  *
  * W, out, in, global_scale, packed_e2m1   as hscale_search.
- * scale_codes   uint8 [out, in / 16], input, each in 1..126; a byte
- *               outside that range is treated as the nearest of 1 and 126.
+ * scale_codes   uint8 [out, in / 16], input, normally each in 1..126.  The
+ *               byte's unsigned value is clipped into 1..126 (0 reads as 1,
+ *               127..255 as 126), the clip the search applies to given
+ *               initial codes, so the result equals the window-0 search from
+ *               those codes (hscale_search_from with down = up = 0).
  */
 int hscale_quantize(const void *W, int64_t out, int64_t in, float global_scale,
                     const uint8_t *scale_codes, uint8_t *packed_e2m1,

@@ -198,9 +198,13 @@ __device__ __forceinline__ void search_group(const float (&w)[kGroup], const flo
         // Every candidate of every lane in the wave is a normal, unclipped
         // code: walk the 8 residue classes c mod 8, each member c + 8 m
         // sharing the products of its class base.  Candidates are then
-        // visited out of order, so ties keep the smaller shift.
+        // visited out of order, so ties keep the smaller shift.  The first
+        // candidate visited always replaces the start state (best_d is above
+        // every shift), so even when every score is +Inf (an fp32 overflow)
+        // the result is a real candidate: the smallest shift, as in the
+        // plain walk.
         float best_e = INFINITY, e_init = 0.0f;
-        int best_d = 0;
+        int best_d = INT_MAX;
         best_p = make_uint2(0u, 0u);
         uint2 p[3] = {best_p, best_p, best_p};
         const int nb = K < 8 ? K : 8;

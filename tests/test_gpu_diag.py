@@ -258,3 +258,43 @@ def test_output_error_70b_shape_sampled(hs):
     Wb = tensor_bits(W[torch.from_numpy(rows).to(DEV)])
     ref = oracle.output_error(Xb, oracle.delta(Wb, s_g, codes[rows], packed[rows]))
     _check_lfull(got.cpu().numpy()[rows], ref, "L_full 70b sampled")
+
+
+def test_shift_summary_hand_worked_on_gpu(hs):
+    """The hand-worked selected-shift case of the oracle pins, through
+    hscale_shift_summary: every bin's count and fp64 sums exactly."""
+    from tests.test_oracle_pins_diag import (HAND_DOWN, HAND_E_BEST, HAND_E_INIT, HAND_SHIFT, HAND_SUMMARY,
+                                             HAND_UP)
+    s = _np(hs.shift_summary(torch.from_numpy(HAND_SHIFT).to(DEV),
+                             torch.from_numpy(HAND_E_BEST.astype(np.float32)).to(DEV),
+                             torch.from_numpy(HAND_E_INIT.astype(np.float32)).to(DEV), HAND_DOWN, HAND_UP))
+    for key, want in HAND_SUMMARY.items():
+        assert np.array_equal(s[key], np.array(want, s[key].dtype)), (key, s[key])
+
+
+def test_shift_summary_exact_groups_on_gpu(hs):
+    """Groups exactly representable at their chosen code only: the GPU's
+    statistics search scores them exactly 0 at that code, and each moved
+    group adds exactly 1 to its bin's relative reduction (groups exact at
+    their initial code add 0)."""
+    from tests.test_oracle_pins_diag import exact_groups
+    s_g = 2.0 ** -10
+    Wb, init = exact_groups(s_g)
+    h32 = np.exp(np.random.default_rng(1).standard_normal(Wb.shape[1])).astype(np.float32)
+    W = torch.from_numpy(Wb.view(np.int16)).view(torch.bfloat16).to(DEV)
+    down = up = 8
+    st = _np(hs.search_stats(W, torch.from_numpy(h32).to(DEV), s_g, down, up,
+                             init=torch.from_numpy(init).to(DEV)))
+    r = oracle.search(Wb, h32, s_g, down=down, up=up, init=init)
+    assert np.array_equal(st["scale_codes"], r["codes"]) and np.array_equal(st["packed_e2m1"], r["packed"])
+    assert np.array_equal(st["shift"], r["shift"])
+    assert np.all(st["err_best"] == 0.0)
+    d = st["shift"].astype(np.int64)
+    assert np.all(st["err_init"][d != 0] > 0) and np.all(st["err_init"][d == 0] == 0)
+    s = _np(hs.shift_summary(torch.from_numpy(st["shift"]).to(DEV), torch.from_numpy(st["err_best"]).to(DEV),
+                             torch.from_numpy(st["err_init"]).to(DEV), down, up))
+    want = np.bincount(d.ravel() + down, minlength=down + up + 1)
+    assert np.array_equal(s["count"], want)
+    rel = want.astype(np.float64)
+    rel[down] = 0.0
+    assert np.array_equal(s["sum_rel"], rel)

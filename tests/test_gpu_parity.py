@@ -226,6 +226,29 @@ def test_quantizer_map_exhaustive(hs):
         assert bad == 0
 
 
+def test_quantize_clips_out_of_range_code_bytes(hs, tiny_case):
+    """Code bytes outside 1..126 (0, the NaN pattern 127, sign-bit bytes
+    128..255) are clipped into the ladder as the header documents: the
+    packed codes equal the oracle's window-0 search from those bytes (the
+    oracle clips given initial codes) and its quantizer at the clipped codes."""
+    W, h, s_g = tiny_case
+    m, n = W.shape
+    rng = np.random.default_rng(3)
+    codes = rng.integers(0, 256, (m, n // 16)).astype(np.uint8)
+    codes[0, :6] = [0, 1, 126, 127, 128, 255]
+    assert np.any(codes == 0) and np.any(codes > 126)
+    packed = hs.quantize(W, s_g, torch.from_numpy(codes).to(DEV)).cpu().numpy()
+    Wb = tensor_bits(W)
+    ref = oracle.search(Wb, h.cpu().numpy(), s_g, down=0, up=0, init=codes)
+    assert np.array_equal(packed, ref["packed"])
+    at, _ = oracle.quantize(Wb, s_g, np.clip(codes, 1, 126).astype(np.uint8))
+    assert np.array_equal(packed, at)
+    # the search from the same bytes at window 0 writes the same bytes
+    c_from, p_from = hs.search(W, h, s_g, window=0, init=torch.from_numpy(codes).to(DEV))
+    assert np.array_equal(p_from.cpu().numpy(), packed)
+    assert np.array_equal(c_from.cpu().numpy(), np.clip(codes, 1, 126))
+
+
 def test_search_deterministic(hs):
     wl = CONFIGS["attn_proj"]
     W = make_weight(wl, DEV)
