@@ -373,8 +373,9 @@ size_t hscale_output_error_workspace_bytes(int64_t tokens, int64_t in,
  * workspace    >= hscale_output_error_workspace_bytes(tokens, in, out)
  *              bytes, 256-byte aligned, scratch owned by the caller (it holds
  *              the two dW planes and per-tile partial sums)
- * in % 16 == 0; global_scale as hscale_search.  tokens, in or out = 0 adds
- * nothing.
+ * in % 16 == 0 and in <= 2^21 (HSCALE_ERR_SHAPE beyond: the kernel
+ * addresses a tile of X and of dW with 32-bit offsets); global_scale as
+ * hscale_search.  tokens, in or out = 0 adds nothing.
  */
 int hscale_output_error(const void *X, int64_t tokens, int64_t in,
                         const void *W, int64_t out, float global_scale,

@@ -161,7 +161,7 @@ __global__ __launch_bounds__(64) void shift_summary_final(const double *__restri
 //
 // dW is formed once in fp32 (w - v S[c], one rounding) and split into two
 // bf16 planes hi + lo (|dW - hi - lo| <= 2^-18 |dW|), so X dW^T is two bf16
-// MFMA products accumulated in fp32.  Each block computes a 256-token x
+// MFMA products accumulated in fp32.  Each block computes a 384-token x
 // 256-row tile of X dW^T in registers and reduces the squares of its columns
 // in fp64; the tile is never written.  Per-tile column sums go to a
 // workspace and a fixed-order tree adds them to row_err.
@@ -171,25 +171,33 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Tile of X dW^T per block: kLfBM tokens x kLfBN weight rows, computed by
-// kLfWM x kLfWN waves (each a (kLfBM / kLfWM) x (kLfBN / kLfWN) sub-tile of
-// 32 x 32 MFMA accumulators).
-constexpr int kLfBM = 256;
+// kLfWM x kLfWN waves (each a 128 x 64 sub-tile of 32 x 32 MFMA
+// accumulators, 128 registers).  Twelve waves, three per SIMD at up to 170
+// registers each: the largest tile the register file holds, which keeps the
+// bytes staged per MFMA flop low (the global -> LDS loads, not the matrix
+// cores, bound this kernel).
+constexpr int kLfBM = 384;
 constexpr int kLfBN = 256;
-constexpr int kLfWM = 2;
+constexpr int kLfWM = 3;
 constexpr int kLfWN = 4;
 constexpr int kLfBK = 32;  // k per LDS stage (two 16-deep MFMA steps)
-constexpr int kLfThreads = 64 * kLfWM * kLfWN;  // two waves per SIMD (launch bounds): 256 registers each
+constexpr int kLfThreads = 64 * kLfWM * kLfWN;
+constexpr int kLfWaves = kLfThreads / 64;
 constexpr int kLfMI = kLfBM / kLfWM / 32;  // accumulator tiles per wave, token direction
 constexpr int kLfNJ = kLfBN / kLfWN / 32;  // accumulator tiles per wave, weight-row direction
 constexpr int kLfRows = kLfBM + 2 * kLfBN;  // LDS rows of 64 bytes per stage (X, dW hi, dW lo)
-constexpr int kLfStages = 3;                // LDS ring depth: two stages in flight while one is used
-constexpr int kLfAhead = kLfStages - 1;     // stages issued ahead of the one being read
-static_assert(kLfStages == 2 || kLfStages == 3, "the vmcnt waits below cover one or two stages ahead");
-constexpr int kLfWaves = kLfThreads / 64;
-constexpr int kLfDmaPerWave = kLfRows / 16 / kLfWaves;  // 1 KB direct-to-LDS loads per wave per stage
-static_assert(kLfRows % (16 * kLfWaves) == 0 && kLfBM % 16 == 0 && kLfBN % 16 == 0, "stage split");
+constexpr int kLfStages = 2;                // LDS ring: one stage in flight while one is read
+constexpr int kLfSlots = kLfRows / 16;      // 1 KB loads per stage, slot q issued by wave q % waves
+constexpr int kLfLoadsPerWave = (kLfSlots + kLfWaves - 1) / kLfWaves;
+static_assert(kLfBM % (kLfWM * 32) == 0 && kLfBN % (kLfWN * 32) == 0, "wave tiles of 32 x 32 accumulators");
 static_assert(kLfStages * kLfRows * 64 <= 160 * 1024, "LDS ring exceeds the CU's 160 KB");
+static_assert(kLfWM * kLfBN * 8 <= kLfRows * 64, "the epilogue's reduction fits in one stage buffer");
 constexpr int64_t kLfMaxTilesPerPass = 1024;  // token tiles per tile launch (bounds the workspace)
+// Buffer descriptors cover one tile's rows with 32-bit byte offsets: every
+// tile spans less than 2^31 bytes for in <= 2^21.
+constexpr int64_t kLfMaxIn = (int64_t)1 << 21;
+constexpr int kLfXcdGroup = 4;  // row tiles grouped per token tile in the XCD-aware order
+constexpr uint32_t kRawBufferWord3 = 0x00020000u;  // raw (untyped) buffer, 32-bit data format
 
 __device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -197,14 +205,12 @@ __device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
 }
 
 // dW of one 16-weight group, split into hi / lo bf16 planes of row stride
-// ldd; groups beyond (out, in) in the padded planes are written as zeros, and
-// so are the 256 bytes at `zero` (the source of out-of-range X chunks).
+// ldd; groups beyond (out, in) in the padded planes are written as zeros.
 __global__ __launch_bounds__(256) void delta_split_kernel(const u32x4 *__restrict__ W, int64_t out, int64_t in,
                                                           float s_g, const uint8_t *__restrict__ codes,
                                                           const uint2 *__restrict__ packed, int64_t rows_pad,
                                                           int64_t ldd, u32x4 *__restrict__ hi,
-                                                          u32x4 *__restrict__ lo, u32x4 *__restrict__ zero) {
-    if (blockIdx.x == 0 && threadIdx.x < 16) zero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+                                                          u32x4 *__restrict__ lo) {
     const int64_t Gp = ldd / kGroup, Gc = in / kGroup;
     const int64_t total = rows_pad * Gp;
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -269,44 +275,86 @@ struct LfArgs {
     int64_t ldd;
     int64_t out;      // weight rows
     int64_t ntiles;   // rows_pad / kLfBN
-    double *partial;    // [token tiles of the pass, out]
-    const u32x4 *zero;  // zeros, read (16 bytes per lane) for chunks outside X
+    double *partial;  // [token tiles of the pass, out]
 };
 
-__global__ __launch_bounds__(kLfThreads, 2) void lfull_tile_kernel(const LfArgs a) {
+// The (token tile, row tile) of block b.  Blocks are dispatched to the 8
+// XCDs round-robin (b % 8); XCD x takes a contiguous range of a linear order
+// in which kLfXcdGroup row tiles of consecutive token tiles are adjacent, so
+// the 32 blocks an XCD runs at once cover about 8 token tiles x 4 row tiles
+// and share their X and dW k-slices in that XCD's L2.  Any order gives the
+// same result; this one minimises the L2 misses of such a rectangle.
+__device__ __forceinline__ void lf_tile_of_block(int64_t b, int64_t total, int64_t ntiles, int64_t &mt,
+                                                 int64_t &nt) {
+    const int64_t per = total / 8, rem = total % 8;
+    const int64_t x = b % 8, slot = b / 8;
+    const int64_t L = x * per + (x < rem ? x : rem) + slot;
+    const int64_t MT = total / ntiles;
+    const int64_t B = ntiles < kLfXcdGroup ? ntiles : kLfXcdGroup;
+    const int64_t full = ntiles / B * B;
+    const int64_t grp = L / (MT * B);
+    if (grp * B < full) {
+        const int64_t r = L - grp * MT * B;
+        mt = r / B;
+        nt = grp * B + r % B;
+    } else {
+        const int64_t Bt = ntiles - full;
+        const int64_t r = L - full * MT;
+        mt = r / Bt;
+        nt = full + r % Bt;
+    }
+}
+
+__global__ __launch_bounds__(kLfThreads, kLfWaves / 4) void lfull_tile_kernel(const LfArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLfStages][kLfRows * 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS addresses in SGPRs
     const int wm = wave % kLfWM, wn = wave / kLfWM;
-    const int64_t mt = blockIdx.x / a.ntiles, nt = blockIdx.x % a.ntiles;
+    int64_t mt, nt;
+    lf_tile_of_block(blockIdx.x, gridDim.x, a.ntiles, mt, nt);
     const int64_t t0 = mt * kLfBM, r0 = nt * kLfBN;
-    const int64_t xrow_vec = a.in / 8, drow_vec = a.ldd / 8;
     const int stages = (int)(a.ldd / kLfBK);
 
-    // A stage is filled straight from global memory into LDS: each wave
-    // issues kLfDmaPerWave 16-byte-per-lane loads, each landing in 1 KB
-    // (16 rows) of the stage, lane l at row 16 kb + l / 4, position l % 4;
-    // the lane fetches the chunk that the swizzle stores at that position.
-    // Rows below kLfBM are X (out-of-range chunks read zeros), then dW hi,
-    // dW lo (padded planes, always in range).
-    auto issue = [&](int s, int buf) {
-        const int64_t kvec = (int64_t)s * (kLfBK / 8);
+    // A stage is loaded straight from global memory into LDS by buffer loads
+    // (16 bytes per lane, 1 KB = 16 rows of the stage per load; lane l at row
+    // 16 q + l / 4, position l % 4, fetching the chunk the swizzle stores
+    // there).  One descriptor per block and operand: the token tile's X rows
+    // (rows past `tokens` lie beyond the descriptor's range and read zeros),
+    // the row tile's dW hi rows and lo rows (padded planes).  Per-lane
+    // 32-bit offsets are fixed for the whole loop; a stage adds a uniform
+    // offset.  X chunks past `in` (when in % 32 != 0) read the next row's
+    // finite values or zeros, and meet zero dW columns.
+    const int64_t xrow_bytes = a.in * 2, drow_bytes = a.ldd * 2;
+    const int64_t valid_rows = a.tokens - t0 < kLfBM ? a.tokens - t0 : kLfBM;
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u32x4 *>(a.X + t0 * (a.in / 8)), 0, (int)(valid_rows * xrow_bytes), kRawBufferWord3);
+    const __amdgpu_buffer_rsrc_t rhi = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u32x4 *>(a.hi + r0 * (a.ldd / 8)), 0, (int)(kLfBN * drow_bytes), kRawBufferWord3);
+    const __amdgpu_buffer_rsrc_t rlo = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u32x4 *>(a.lo + r0 * (a.ldd / 8)), 0, (int)(kLfBN * drow_bytes), kRawBufferWord3);
+    uint32_t voff[kLfLoadsPerWave];
 #pragma unroll
-        for (int i = 0; i < kLfDmaPerWave; ++i) {
-            const int kb = wave + i * kLfWaves;
-            const int row = kb * 16 + (lane >> 2);
-            const int c = (lane & 3) ^ ((row >> 2) & 3);
-            const u32x4 *src;
-            if (kb < kLfBM / 16) {
-                const int64_t t = t0 + row, kv = kvec + c;
-                src = (t < a.tokens && kv < xrow_vec) ? a.X + t * xrow_vec + kv : a.zero;
-            } else {
-                const int rb = row - kLfBM;
-                const u32x4 *plane = rb < kLfBN ? a.hi : a.lo;
-                src = plane + (r0 + rb % kLfBN) * drow_vec + kvec + c;
+    for (int i = 0; i < kLfLoadsPerWave; ++i) {
+        const int q = wave + i * kLfWaves;
+        const int row = q * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ ((row >> 2) & 3);
+        voff[i] = row < kLfBM ? (uint32_t)(row * xrow_bytes + c * 16)
+                              : (uint32_t)(((row - kLfBM) % kLfBN) * drow_bytes + c * 16);
+    }
+    auto issue = [&](int s, int buf) {
+        const uint32_t soff = (uint32_t)s * (kLfBK * 2);
+#pragma unroll
+        for (int i = 0; i < kLfLoadsPerWave; ++i) {
+            const int q = wave + i * kLfWaves;
+            if (q < kLfSlots) {
+                auto *dst = (__attribute__((address_space(3))) void *)(lds[buf] + q * 1024);
+                if (q < kLfBM / 16)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, dst, 16, voff[i], soff, 0, 0);
+                else if (q < (kLfBM + kLfBN) / 16)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rhi, dst, 16, voff[i], soff, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rlo, dst, 16, voff[i], soff, 0, 0);
             }
-            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src),
-                                             (__attribute__((address_space(3))) void *)(lds[buf] + kb * 1024), 16,
-                                             0, 0);
         }
     };
 
@@ -318,23 +366,17 @@ __global__ __launch_bounds__(kLfThreads, 2) void lfull_tile_kernel(const LfArgs 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    // Ring of kLfStages buffers, kLfAhead = kLfStages - 1 stages ahead: stage
-    // s + kLfAhead is issued once every wave has finished reading stage s - 1
-    // (the barrier), into that stage's buffer.  Each wave first waits for its
-    // own loads of stage s (vmcnt counts them in issue order; the loads of
-    // the later stages may stay in flight); the barrier then makes all of
-    // stage s visible.  A plain s_barrier is used: __syncthreads() adds a
-    // release fence that waits for every outstanding load.
-#pragma unroll
-    for (int p = 0; p < kLfAhead; ++p)
-        if (p < stages) issue(p, p);
+    // Two-buffer ring: stage s + 1 is issued once every wave has finished
+    // reading stage s - 1 (the barrier), into that stage's buffer.  Each wave
+    // first waits for its own loads of stage s (all its outstanding loads),
+    // then the barrier makes all of stage s visible.  A plain s_barrier is
+    // used: __syncthreads() adds a release fence that waits for every
+    // outstanding load, the stage just issued included.
+    issue(0, 0);
     for (int s = 0; s < stages; ++s) {
-        if (kLfAhead > 1 && s + 1 < stages)
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLfDmaPerWave));
-        else
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
         asm volatile("s_barrier" ::: "memory");
-        if (s + kLfAhead < stages) issue(s + kLfAhead, (s + kLfAhead) % kLfStages);
+        if (s + 1 < stages) issue(s + 1, (s + 1) % kLfStages);
         const uint8_t *base = lds[s % kLfStages];
 #pragma unroll
         for (int kk = 0; kk < kLfBK / 16; ++kk) {
@@ -395,7 +437,7 @@ __global__ __launch_bounds__(kLfThreads, 2) void lfull_tile_kernel(const LfArgs 
 
 struct LfPlan {
     int64_t ldd = 0, rows_pad = 0, ntiles = 0, tiles_per_pass = 0;
-    size_t plane_bytes = 0, zero_offset = 0, partial_offset = 0, bytes = 0;
+    size_t plane_bytes = 0, partial_offset = 0, bytes = 0;
 };
 
 LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
@@ -411,8 +453,7 @@ LfPlan lfull_plan(int64_t tokens, int64_t in, int64_t out) {
     const int64_t cap = grid_cap < kLfMaxTilesPerPass ? grid_cap : kLfMaxTilesPerPass;
     p.tiles_per_pass = tiles < cap ? tiles : cap;
     p.plane_bytes = round_up((size_t)p.rows_pad * (size_t)p.ldd * 2, 256);
-    p.zero_offset = 2 * p.plane_bytes;
-    p.partial_offset = p.zero_offset + 256;
+    p.partial_offset = 2 * p.plane_bytes;
     p.bytes = p.partial_offset + (size_t)p.tiles_per_pass * (size_t)out * sizeof(double);
     return p;
 }
@@ -475,7 +516,7 @@ int hscale_shift_summary(const int8_t *shift, const float *err_best, const float
 }
 
 size_t hscale_output_error_workspace_bytes(int64_t tokens, int64_t in, int64_t out) {
-    if (in % kGroup != 0 || in > ((int64_t)1 << 40) || (in > 0 && out > kMaxGroups / (in / kGroup))) return 0;
+    if (in % kGroup != 0 || in > kLfMaxIn || (in > 0 && out > kMaxGroups / (in / kGroup))) return 0;
     return lfull_plan(tokens, in, out).bytes;
 }
 
@@ -483,7 +524,7 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
                         const uint8_t *scale_codes, const uint8_t *packed_e2m1, double *row_err, void *workspace,
                         size_t workspace_bytes, hipStream_t stream) {
     if (tokens < 0 || in < 0 || out < 0 || in % kGroup != 0) return HSCALE_ERR_SHAPE;
-    if (in > ((int64_t)1 << 40) || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
+    if (in > kLfMaxIn || (in > 0 && tokens > ((int64_t)1 << 46) / in)) return HSCALE_ERR_SHAPE;
     if (in > 0 && out > kMaxGroups / (in / kGroup)) return HSCALE_ERR_SHAPE;
     if (!scale_ok(global_scale)) return HSCALE_ERR_SCALE;
     if (tokens == 0 || in == 0 || out == 0) return HSCALE_OK;  // adds nothing
@@ -509,8 +550,7 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
     double *partial = reinterpret_cast<double *>(ws + p.partial_offset);
     hipLaunchKernelGGL(delta_split_kernel, dim3(grid_for(p.rows_pad * (p.ldd / kGroup), 256)), dim3(256), 0, stream,
                        static_cast<const u32x4 *>(W), out, in, global_scale, scale_codes,
-                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo,
-                       reinterpret_cast<u32x4 *>(ws + p.zero_offset));
+                       reinterpret_cast<const uint2 *>(packed_e2m1), p.rows_pad, p.ldd, hi, lo);
     if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;
     const int64_t pass_tokens = p.tiles_per_pass * kLfBM;
     for (int64_t t0 = 0; t0 < tokens; t0 += pass_tokens) {
@@ -524,7 +564,6 @@ int hscale_output_error(const void *X, int64_t tokens, int64_t in, const void *W
         a.out = out;
         a.ntiles = p.ntiles;
         a.partial = partial;
-        a.zero = reinterpret_cast<const u32x4 *>(ws + p.zero_offset);
         const int64_t tiles = (a.tokens + kLfBM - 1) / kLfBM;
         hipLaunchKernelGGL(lfull_tile_kernel, dim3((unsigned)(tiles * p.ntiles)), dim3(kLfThreads), 0, stream, a);
         if (launch_status() != HSCALE_OK) return HSCALE_ERR_HIP;

@@ -263,6 +263,10 @@ def test_output_error_validation(L):
     assert oe(n=17) == -2
     assert oe(T=-1) == -2
     assert oe(m=-3) == -2
+    # a tile of X is addressed with 32-bit offsets: in <= 2^21
+    assert L.hscale_output_error_workspace_bytes(T, 2 ** 21 + 16, 1) == 0
+    assert L.hscale_output_error_workspace_bytes(1, 2 ** 21, 1) > 0
+    assert oe(n=2 ** 21 + 16, m=1, T=1) == -2
     assert oe(s=0.0) == -5
     assert oe(X=0) == -1
     assert oe(row=0) == -1

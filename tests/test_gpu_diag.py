@@ -207,9 +207,9 @@ def test_output_error_accumulates_and_code_zero(hs):
 
 
 def test_output_error_two_passes(hs):
-    """More tokens than one tile launch covers (1024 tiles of 256): the
+    """More tokens than one tile launch covers (1024 token tiles of 384): the
     second pass adds its partials to the first."""
-    T, n, m = 262144 + 300, 64, 96
+    T, n, m = 1024 * 384 + 300, 64, 96
     W, X, Wb, Xb, s_g, codes, packed = _lfull_case(hs, T, n, m, seed=2)
     got = hs.output_error(X.to(DEV), W.to(DEV), s_g, torch.from_numpy(codes).to(DEV),
                           torch.from_numpy(packed).to(DEV))
