@@ -21,9 +21,10 @@ Cache, so the search reads W from HBM.
 
 Prints one JSON line.  `value` is the search throughput in Gweights/s (the
 metric's first figure); `hdiag` carries the second figure (HBM GB/s and its
-fraction of the 8 TB/s peak).  `cpu_baseline` is the CPU oracle timed on a
-bounded sample of the same workload on this host; the same sample is checked
-for parity against the benchmarked outputs.
+fraction of the 8 TB/s peak).  `cpu_baseline` is the CPU oracle timed on this
+host's cores over the same workload's last layer (its whole W and X by
+default); the same rows and tokens are checked for parity against the
+benchmarked outputs.
 """
 from __future__ import annotations
 
@@ -43,14 +44,11 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 # fp32 VALU issue ceiling: 256 CU x 4 SIMD x 32 lanes/clk (one wave64 fp32
 # op per 2 clocks) x 2.4 GHz = 78.64 T lane-ops/s = 157.3 TFLOP/s of FMA.
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
-# Two further reference rates for the search, reported beside the peak:
-# a 16-lane-per-SIMD issue model (one wave64 instruction per 4 clocks), which
-# measured fp32 FMA throughput exceeds, so it is not a ceiling; and the
-# ceiling of the search's own instruction mix at measured per-class issue
-# costs (4 fp32 operations at 1.21 ns plus half a 3.50 ns FP4 pack and half
-# a 1.99 ns FP4 unpack conversion per weight-candidate, per wave per SIMD).
+# The 16-lane issue model first proposed for the search (one wave64 fp32
+# instruction per 4 clocks per SIMD), reported beside the peak; the search
+# issues VALU instructions faster than that (committed counters), so it is
+# not a ceiling.
 ISSUE16_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-MIX_CEILING_TOPS = 5 * 64 * 1024 / (4 * 1.21 + 3.50 / 2 + 1.99 / 2) / 1e3
 SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
 HERE = os.path.dirname(os.path.abspath(__file__))
 # Sources of the hot-path kernels (hdiag, search): the committed HBM-traffic
@@ -123,7 +121,7 @@ def measured_traffic(workload: str):
         return sum(per_step(n) for n in names)
     search = "search_layers_kernel" if "search_layers_kernel" in t else "search_kernel"
     return {"hdiag": tot("hdiag_partial", "hdiag_tree"), "search": tot(search),
-            "source": os.path.relpath(path, HERE)}
+            "valu": prof.get("valu", {}).get(search), "source": os.path.relpath(path, HERE)}
 
 
 def parse():
@@ -137,10 +135,10 @@ def parse():
     ap.add_argument("--down", type=int, default=None, help="asymmetric shift set -down..+up")
     ap.add_argument("--up", type=int, default=None)
     ap.add_argument("--init", default="maxabs", choices=["maxabs", "4over6"])
-    ap.add_argument("--cpu-rows", type=int, default=3072,
-                    help="rows of W in the CPU oracle sample (also checked for parity)")
-    ap.add_argument("--cpu-tokens", type=int, default=65536,
-                    help="tokens of X in the CPU oracle hdiag sample")
+    ap.add_argument("--cpu-rows", type=int, default=None,
+                    help="rows of W in the CPU oracle leg (default: all; also checked for parity)")
+    ap.add_argument("--cpu-tokens", type=int, default=None,
+                    help="tokens of X in the CPU oracle hdiag leg (default: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-diagnostics", action="store_true",
                     help="skip the quality-diagnostics leg (shift statistics, Eq. 3 output error)")
@@ -178,6 +176,11 @@ def build_workload(name, dev, window_override):
     return acts, layers, desc
 
 
+def progress(msg: str) -> None:
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -201,6 +204,7 @@ def main():
     dev = "cuda"
     torch.cuda.set_device(0)
 
+    progress(f"generating the {args.workload} workload")
     acts, layers, desc = build_workload(args.workload, dev, args.window)
     if args.down is not None:
         layers = [(l, W, xk, s, None) for (l, W, xk, s, _) in layers]
@@ -246,6 +250,7 @@ def main():
             evs[k + 1].record(stream)
 
     n_ev = len(acts) + 2
+    progress(f"{args.warmup} warm-up and {args.steps} timed steps")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -290,8 +295,6 @@ def main():
     rl_search = {"bound": "alu", "achieved": round(search_tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
                  "unit": "T lane-ops/s", "frac": round(search_tops / VALU_PEAK_TOPS, 4), "traffic": None,
                  "frac_of_16_lane_issue_model": round(search_tops / ISSUE16_TOPS, 4),
-                 "frac_of_mix_ceiling": round(search_tops / MIX_CEILING_TOPS, 4),
-                 "mix_ceiling": round(MIX_CEILING_TOPS, 2),
                  "kernel": "hscale_search (search_kernel)",
                  "algorithmic_ops_per_step": ops, "hbm_GBps": round(search_gbs, 1),
                  "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
@@ -303,6 +306,9 @@ def main():
         rl_hdiag["traffic"] = traffic["hdiag"]
         rl_search["traffic"] = traffic["search"]
         rl_hdiag["traffic_source"] = rl_search["traffic_source"] = traffic["source"]
+        if traffic["valu"]:
+            # VALU issue counters of the search kernel from the same summary
+            rl_search["valu_counters"] = dict(traffic["valu"], source=traffic["source"])
     dominant = rl_hdiag if t_h.mean() >= t_s.mean() else rl_search
 
     out = {
@@ -328,7 +334,6 @@ def main():
         "search_isolated": None if iso is None else {
             "Gweights_per_s": round(weights / iso / 1e9, 2), "ms": round(iso * 1e3, 4),
             "frac_of_valu_roofline": round(ops / iso / 1e12 / VALU_PEAK_TOPS, 4),
-            "frac_of_mix_ceiling": round(ops / iso / 1e12 / MIX_CEILING_TOPS, 4),
             "protocol": "the step's search call alone: 3 warm-ups, then the median of 20 runs, a 1 GiB device "
                         "buffer overwritten before each run; not the headline (the step runs the search right "
                         "after the hdiag read, at a lower engine clock)"},
@@ -338,8 +343,10 @@ def main():
         "rooflines": {"hdiag": rl_hdiag, "search": rl_search},
     }
     if not args.no_cpu_baseline:
+        progress("CPU oracle leg and parity")
         out.update(cpu_leg(args, acts, layers))
     if not args.no_diagnostics:
+        progress("diagnostics leg")
         out["diagnostics"] = diag_leg(args, acts, layers)
     print(json.dumps(out), flush=True)
 
@@ -460,14 +467,21 @@ def diag_leg(args, acts, layers, repeats=5):
 
 
 def cpu_leg(args, acts, layers):
-    """The oracle on a bounded sample of the same workload, on this host's
-    cores: rows of the last layer's W and tokens of its X.
+    """The oracle on this host's cores, on the workload's last layer: by
+    default its whole W and whole X (the full configuration), else the first
+    --cpu-rows rows and --cpu-tokens tokens.
 
-    Parity: h for the check is the oracle's, over the sampled tokens, rounded
+    All cores: the rows (tokens) split into one contiguous chunk per core,
+    one unmodified oracle call per chunk on its own thread (the oracle's C
+    code shares no state between calls and ctypes releases the GIL), timed
+    wall-clock.  One thread: a fixed 256-row search slice and an 8192-token
+    hdiag slice, extrapolated linearly to the same size and labelled so.
+
+    Parity: h for the check is the oracle's, over the same tokens, rounded
     to fp32 (no oracle input comes from the HIP path).  The HIP search runs
     again, untimed, on the whole last layer in the launch configuration the
-    timed steps use, with that h; its sampled rows must match the oracle's
-    search.  The HIP hdiag of the sampled tokens is checked against the
+    timed steps use, with that h; every checked row must match the oracle's
+    search.  The HIP hdiag of the same tokens is checked against the
     oracle's h."""
     import torch
     import paper_2608_28113_amd as hs
@@ -477,54 +491,70 @@ def cpu_leg(args, acts, layers):
 
     lname, W, xk, s_g, w = layers[-1]
     X = acts[xk]
-    rows = min(args.cpu_rows, W.shape[0])
-    tok = min(args.cpu_tokens, X.shape[0])
+    rows = W.shape[0] if args.cpu_rows is None else min(args.cpu_rows, W.shape[0])
+    tok = X.shape[0] if args.cpu_tokens is None else min(args.cpu_tokens, X.shape[0])
+    full = rows == W.shape[0] and tok == X.shape[0]
     down, up = (w, w) if w is not None else (args.down, args.up)
     init = "4over6" if args.init == "4over6" else "rtn"
     Wb = tensor_bits(W[:rows])
     Xb = tensor_bits(X[:tok])
     oracle._load()
-    t0 = time.perf_counter()
-    href = oracle.hdiag(Xb)
-    t_hd = time.perf_counter() - t0
-    h_in = href.astype(np.float32)
-    t0 = time.perf_counter()
-    ref = oracle.search(Wb, h_in, s_g, down=down, up=up, init=init)
-    t_search = time.perf_counter() - t0
-    # The same sample on all of this host's cores: contiguous row (token)
-    # chunks, one oracle call per core.  The oracle's C code shares no state
-    # between calls and ctypes releases the GIL while it runs.
     cores = _host_cores()
+
+    # one thread, fixed slices
+    r1, t1 = min(256, rows), min(8192, tok)
+    t0 = time.perf_counter()
+    h1 = oracle.hdiag(Xb[:t1])
+    t_hd1 = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.search(Wb[:r1], h1.astype(np.float32), s_g, down=down, up=up, init=init)
+    t_s1 = time.perf_counter() - t0
+
+    # all cores, the whole sample
     row_sl = [sl for sl in np.array_split(np.arange(rows), cores) if len(sl)]
     tok_sl = [sl for sl in np.array_split(np.arange(tok), cores) if len(sl)]
     with ThreadPoolExecutor(max_workers=cores) as ex:
         t0 = time.perf_counter()
-        list(ex.map(lambda sl: oracle.hdiag(Xb[sl[0]:sl[-1] + 1]), tok_sl))
-        t_hd_all = time.perf_counter() - t0
+        parts = list(ex.map(lambda sl: oracle.hdiag(Xb[sl[0]:sl[-1] + 1]), tok_sl))
+        t_hd = time.perf_counter() - t0
+        href = np.sum(parts, axis=0)  # fp64 sum of the chunk sums
+        h_in = href.astype(np.float32)
         t0 = time.perf_counter()
-        list(ex.map(lambda sl: oracle.search(Wb[sl[0]:sl[-1] + 1], h_in, s_g, down=down, up=up, init=init),
-                    row_sl))
-        t_search_all = time.perf_counter() - t0
+        res = list(ex.map(lambda sl: oracle.search(Wb[sl[0]:sl[-1] + 1], h_in, s_g, down=down, up=up,
+                                                   init=init), row_sl))
+        t_search = time.perf_counter() - t0
+    ref = {k: np.concatenate([r[k] for r in res]) for k in res[0]}
+
     codes, packed = hs.search(W, torch.from_numpy(h_in).to(W.device), s_g, down=down, up=up, init=args.init)
     rep = parity.compare_search(Wb, h_in, s_g, down, up, codes[:rows].cpu().numpy(), packed[:rows].cpu().numpy(),
                                 init=init, oracle_result=ref)
-    h_slice = hs.hdiag(X[:tok].contiguous()).cpu().numpy()
-    hrep = parity.compare_h(h_slice, href)
+    h_gpu = hs.hdiag(X if tok == X.shape[0] else X[:tok].contiguous()).cpu().numpy()
+    hrep = parity.compare_h(h_gpu, href)
+    what = (f"the full {lname} configuration: search of all {rows} rows ({Wb.size} weights, shifts -{down}..+{up}, "
+            f"init {init}), hdiag of all {tok} tokens of its X ({Xb.nbytes / 1e9:.2f} GB)") if full else (
+            f"rows 0..{rows - 1} of {lname} ({Wb.size} weights, shifts -{down}..+{up}, init {init}); "
+            f"tokens 0..{tok - 1} of its X ({Xb.nbytes / 1e9:.2f} GB)")
     return {
         "cpu_baseline": {
-            "value": round(Wb.size / t_search / 1e9, 6), "unit": "Gweights/s", "cores": 1, "kind": "oracle",
-            "sample": f"search on rows 0..{rows - 1} of {lname} ({Wb.size} weights, shifts -{down}..+{up}, "
-                      f"init {init}, {t_search:.2f} s); hdiag on tokens 0..{tok - 1} of its X "
-                      f"({Xb.nbytes / 1e9:.2f} GB, {t_hd:.2f} s, {Xb.nbytes / t_hd / 1e9:.2f} GB/s)",
+            "value": round(Wb.size / t_search / 1e9, 6), "unit": "Gweights/s", "cores": len(row_sl),
+            "kind": "oracle",
+            "sample": f"{what}; {len(row_sl)} threads, one oracle call per contiguous chunk; search "
+                      f"{t_search:.2f} s, hdiag {t_hd:.2f} s",
+            "full_config": full,
             "hdiag_GBps": round(Xb.nbytes / t_hd / 1e9, 3),
+            "search_s": round(t_search, 3), "hdiag_s": round(t_hd, 3),
             "cpu_model": _cpu_model(),
             "host_cpus": os.cpu_count(),
-            "all_cores": {"value": round(Wb.size / t_search_all / 1e9, 6), "unit": "Gweights/s", "cores": cores,
-                          "hdiag_GBps": round(Xb.nbytes / t_hd_all / 1e9, 3),
-                          "sample": f"the same rows and tokens in {len(row_sl)} and {len(tok_sl)} contiguous "
-                                    f"chunks, one oracle call per core ({t_search_all:.2f} s, {t_hd_all:.2f} s)"},
+            "one_thread": {
+                "value": round(r1 * Wb.shape[1] / t_s1 / 1e9, 6), "unit": "Gweights/s", "cores": 1,
+                "hdiag_GBps": round(t1 * Xb.shape[1] * 2 / t_hd1 / 1e9, 3),
+                "extrapolated": True,
+                "search_s_extrapolated": round(t_s1 * rows / r1, 2),
+                "hdiag_s_extrapolated": round(t_hd1 * tok / t1, 2),
+                "sample": f"rows 0..{r1 - 1} ({t_s1:.2f} s) and tokens 0..{t1 - 1} ({t_hd1:.3f} s) on one "
+                          f"thread, extrapolated linearly to the {rows} rows and {tok} tokens above"},
         },
-        "parity": {"layer": lname, "h_source": f"oracle hdiag of tokens 0..{tok - 1}, fp32",
+        "parity": {"layer": lname, "h_source": f"oracle hdiag of tokens 0..{tok - 1} (chunk sums in fp64), fp32",
                    "search_rows_checked": rows, "groups": rep["groups"],
                    "near_ties": rep["near_ties"], "init_ties": rep["init_ties"], "mismatches": rep["mismatches"],
                    "ok": rep["ok"], "hdiag_tokens_checked": tok, "hdiag_max_rel": hrep["max_rel"],

@@ -1,6 +1,7 @@
 """bench.py on the CPU: its command-line contract (more than one GPU is
 refused with a message before anything touches a GPU, inconsistent window
-flags are rejected), and the committed profiles it quotes."""
+flags are rejected), and the committed profiles it quotes, which must be
+current for the kernel sources."""
 import subprocess
 import sys
 from pathlib import Path
@@ -37,8 +38,9 @@ def test_committed_profile_traffic_matches_the_algorithmic_bytes(workload):
     from synth.workloads import CONFIGS, block_workloads
 
     t = bench.measured_traffic(workload)
-    if t is None:
-        pytest.skip(f"profiles/{workload}.json is absent or older than the kernel sources")
+    # A missing or stale summary fails: the bench line would silently lose
+    # its measured traffic.  Re-collect the profile after a kernel change.
+    assert t is not None, f"profiles/{workload}.json is absent or older than the kernel sources"
     if workload == "block":
         wls = block_workloads()
         # X_attn and X_mlp (262144 x 4096) and X_down (262144 x 14336)
