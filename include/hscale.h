@@ -141,7 +141,9 @@ int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
  * 8 MiB are rejected with HSCALE_ERR_SCRATCH before anything is enqueued;
  * every in <= 2^20 (any tokens) fits.  The first call on a device looks up
  * that device's copy of the array (hipGetSymbolAddress) and keeps its
- * address; a failed lookup returns HSCALE_ERR_HIP.
+ * address; a failed lookup returns HSCALE_ERR_HIP.  That lookup is a runtime
+ * call: make the first call on each device outside stream capture (later
+ * calls, captured or not, only enqueue kernels).
  *
  * All calls on one GPU share that GPU's array: calls that may run at the
  * same time on one GPU (different streams, or host threads that do not

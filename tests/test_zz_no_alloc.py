@@ -83,3 +83,57 @@ def test_noalloc_zero_tokens_and_size_limit(L):
     n = (1 << 20) + 16
     assert L.hscale_hdiag_workspace_bytes(1024, n) > SCRATCH_BYTES
     assert L.hscale_hdiag_noalloc(1 << 20, 1024, n, 1 << 40, stream) == -9
+
+
+def test_noalloc_replays_in_a_graph(L):
+    """The callers this entry point is for include code under HIP graph
+    capture: hdiag_noalloc and the search captured together (no buffer is
+    allocated during capture, the scratch included), replayed four times;
+    between replays an eager hdiag_noalloc of another, smaller X overwrites
+    the shared scratch.  Every replay equals the eager results bit for bit."""
+    import paper_2608_28113_amd as hs
+    from synth.workloads import harness_global_scale, make_weight
+    wl = CONFIGS["attn_proj"]
+    X = make_activations(wl, DEV, tokens=8192, n=2048)
+    X2 = make_activations(wl, DEV, tokens=700, n=1040)
+    W = make_weight(wl, DEV, shape=(512, 2048))
+    s_g = harness_global_scale(W)
+    T, n = X.shape
+    m = W.shape[0]
+    h = torch.empty(n, dtype=torch.float32, device=DEV)
+    h2 = torch.empty(X2.shape[1], dtype=torch.float32, device=DEV)
+    codes = torch.empty((m, n // 16), dtype=torch.uint8, device=DEV)
+    packed = torch.empty((m, n // 2), dtype=torch.uint8, device=DEV)
+
+    def step(stream):
+        assert L.hscale_hdiag_noalloc(X.data_ptr(), T, n, h.data_ptr(), stream.cuda_stream) == 0
+        hs.search(W, h, s_g, down=9, up=6, scale_codes=codes, packed_e2m1=packed, stream=stream)
+
+    step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    ref = (h.clone(), codes.clone(), packed.clone())
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        step(side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(torch.cuda.current_stream())
+    for i in range(4):
+        h.zero_()
+        codes.zero_()
+        packed.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((h, codes, packed), ref):
+            assert torch.equal(got, want), f"replay {i}"
+        # eager work between replays that reuses the scratch
+        stream = torch.cuda.current_stream().cuda_stream
+        assert L.hscale_hdiag_noalloc(X2.data_ptr(), X2.shape[0], X2.shape[1], h2.data_ptr(), stream) == 0
+        torch.cuda.synchronize()
+    assert parity.compare_h(h2.cpu().numpy(), oracle.hdiag(tensor_bits(X2)))["ok"]
