@@ -21,7 +21,10 @@ Cache, so the search reads W from HBM.
 
 Prints one JSON line.  `value` is the search throughput in Gweights/s (the
 metric's first figure); `hdiag` carries the second figure (HBM GB/s and its
-fraction of the 8 TB/s peak).  `cpu_baseline` is the CPU oracle timed on this
+fraction of the 8 TB/s peak).  `ceilings` holds what the chip sustains in the
+same run for the same kinds of work (a streaming read, VALU issue of the
+search's instruction stream), measured by the probes of libhscale_probes.so
+after the timed steps; the rooflines carry each kernel's fraction of them.  `cpu_baseline` is the CPU oracle timed on this
 host's cores over the same workload's last layer (its whole W and X by
 default); the same rows and tokens are checked for parity against the
 benchmarked outputs.
@@ -44,13 +47,9 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 # fp32 VALU issue ceiling: 256 CU x 4 SIMD x 32 lanes/clk (one wave64 fp32
 # op per 2 clocks) x 2.4 GHz = 78.64 T lane-ops/s = 157.3 TFLOP/s of FMA.
 VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
-# The 16-lane issue model first proposed for the search (one wave64 fp32
-# instruction per 4 clocks per SIMD), reported beside the peak; the search
-# issues VALU instructions faster than that (committed counters), so it is
-# not a ceiling.
-ISSUE16_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 SEARCH_BYTES_PER_WEIGHT = 2 + 0.5 + 1.0 / 16  # read W, write codes and scales
 HERE = os.path.dirname(os.path.abspath(__file__))
+PROBE_LIB = os.path.join(HERE, "paper_2608_28113_amd", "libhscale_probes.so")
 # Sources of the hot-path kernels (hdiag, search): the committed HBM-traffic
 # figures are valid only for the source they were measured on.
 HOT_SOURCES = ("common.h", "hdiag.hip", "search.hip")
@@ -140,6 +139,8 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=None,
                     help="tokens of X in the CPU oracle hdiag leg (default: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured read and VALU ceilings (probe kernels run after the timed steps)")
     ap.add_argument("--no-diagnostics", action="store_true",
                     help="skip the quality-diagnostics leg (shift statistics, Eq. 3 output error)")
     ap.add_argument("--diag-profile", action="store_true",
@@ -294,12 +295,23 @@ def main():
                 "launches_per_step": nh}
     rl_search = {"bound": "alu", "achieved": round(search_tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
                  "unit": "T lane-ops/s", "frac": round(search_tops / VALU_PEAK_TOPS, 4), "traffic": None,
-                 "frac_of_16_lane_issue_model": round(search_tops / ISSUE16_TOPS, 4),
                  "kernel": "hscale_search (search_kernel)",
                  "algorithmic_ops_per_step": ops, "hbm_GBps": round(search_gbs, 1),
                  "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
                  "launches_per_step": 1 if len(layers) <= 32 else (len(layers) + 31) // 32,
                  "layers": len(layers)}
+    ceil = None
+    if not args.no_ceilings:
+        progress("measured ceilings (streaming read, VALU issue)")
+        ceil = ceilings_leg(max(acts.values(), key=lambda X: X.numel()), stream)
+        rl_hdiag["frac_of_stream_read"] = round(hd_gbs / ceil["stream_read"]["GBps"], 4)
+        wc = sum(W.numel() * (2 * w + 1 if w is not None else args.down + args.up + 1)
+                 for (_, W, _, _, w) in layers)
+        mix = ceil["valu"]["search_pair_weight_candidates_per_s"]
+        rl_search["weight_candidates_per_s"] = wc / t_s.mean()
+        rl_search["frac_of_search_mix"] = round(wc / t_s.mean() / mix, 4)
+        if iso is not None:
+            rl_search["frac_of_search_mix_isolated"] = round(wc / iso / mix, 4)
     default_shape = args.init == "maxabs" and args.down is None and args.window is None
     traffic = measured_traffic(args.workload) if default_shape else None
     if traffic:
@@ -341,6 +353,7 @@ def main():
         "wall_s_timed": round(wall, 4),
         "roofline": dominant,
         "rooflines": {"hdiag": rl_hdiag, "search": rl_search},
+        "ceilings": ceil,
     }
     if not args.no_cpu_baseline:
         progress("CPU oracle leg and parity")
@@ -372,6 +385,98 @@ def isolated_search(run_search, stream):
     torch.cuda.synchronize()
     del flush
     return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e-3
+
+
+def load_probes():
+    """libhscale_probes.so: the measurement probes (built beside libhscale.so)."""
+    import ctypes
+
+    if not os.path.exists(PROBE_LIB):
+        raise RuntimeError(f"{PROBE_LIB} is not built: run `python __graft_entry__.py build`")
+    lib = ctypes.CDLL(PROBE_LIB)
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.hsprobe_stream_read.argtypes = [P, i64, i32, P, P]
+    lib.hsprobe_stream_read.restype = i64
+    lib.hsprobe_valu.argtypes = [i32, i32, i32, P, P, P]
+    lib.hsprobe_valu.restype = ctypes.c_int
+    lib.hsprobe_wall_clock_khz.argtypes = []
+    lib.hsprobe_wall_clock_khz.restype = ctypes.c_int
+    return lib
+
+
+# hsprobe_valu kinds: (name, loop iterations, VALU instructions per iteration)
+VALU_PROBES = {0: ("fma", 1024, 64), 1: ("pack_cvt", 256, 64), 2: ("unpack_cvt", 512, 64),
+               3: ("search_pair", 512, None)}
+READ_PROBE_BLOCKS = 1792  # as many blocks as the chip keeps resident (256 CUs x 7)
+
+
+def ceilings_leg(X, stream):
+    """What this MI355X sustains, measured in the same run, for the two kinds
+    of work on the path:
+      stream_read  a read of the largest activation tensor with 16-byte
+                   non-temporal loads (the median of 5), against which hdiag's
+                   rate is set (frac_of_stream_read);
+      valu         VALU issue from registers with no memory traffic: plain fp32
+                   FMAs, the FP4 pack and unpack conversions (cycles per wave64
+                   instruction per SIMD at the clock read from s_memtime /
+                   s_memrealtime), and the scale search's per-candidate
+                   instruction stream (two candidates of a 16-weight group per
+                   iteration), whose weight-candidates per second the search's
+                   own rate is set against (frac_of_search_mix).  7 waves per
+                   SIMD, the search kernel's occupancy."""
+    import torch
+
+    lib = load_probes()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    simds = 4 * cus
+
+    def timed(fn, runs):
+        ts, r = [], None
+        for i in range(runs + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            r = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if i:  # the first run is a warm-up
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+        return float(np.median(ts)), r
+
+    sums = torch.empty(READ_PROBE_BLOCKS * 256, dtype=torch.int32, device=X.device)
+    t_read, nread = timed(lambda: lib.hsprobe_stream_read(X.data_ptr(), X.numel() * X.element_size(),
+                                                          READ_PROBE_BLOCKS, sums.data_ptr(), stream.cuda_stream), 5)
+    if nread <= 0:
+        raise RuntimeError("hsprobe_stream_read failed")
+    read_gbs = nread / t_read / 1e9
+
+    wall_hz = lib.hsprobe_wall_clock_khz() * 1e3
+    blocks = 7 * cus
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device=X.device)
+    clocks = torch.zeros(blocks * 4 * 4, dtype=torch.int64, device=X.device)
+    valu = {"blocks": blocks, "waves_per_simd": 7}
+    ghz = []
+    for kind, (name, iters, per_iter) in VALU_PROBES.items():
+        t, st = timed(lambda: lib.hsprobe_valu(kind, blocks, iters, sink.data_ptr(), clocks.data_ptr(),
+                                               stream.cuda_stream), 3)
+        if st != 0:
+            raise RuntimeError(f"hsprobe_valu({kind}) failed")
+        c = clocks.view(-1, 4).cpu().numpy().astype(np.float64)
+        clock = float(np.median((c[:, 1] - c[:, 0]) / (c[:, 3] - c[:, 2]))) * wall_hz
+        ghz.append(clock / 1e9)
+        if per_iter is not None:
+            instr_per_simd = blocks * 4 * iters * per_iter / simds
+            valu[f"{name}_cycles_per_instr_per_simd"] = round(t * clock / instr_per_simd, 3)
+            if name == "fma":
+                valu["fma_T_lane_ops_per_s"] = round(blocks * 256 * iters * per_iter / t / 1e12, 2)
+        else:
+            valu["search_pair_weight_candidates_per_s"] = blocks * 256 * iters * 2 * 16 / t
+            valu["search_pair_ms"] = round(t * 1e3, 4)
+    valu["clock_GHz"] = [round(g, 3) for g in ghz]
+    valu["clock_source"] = "median over waves of the s_memtime / s_memrealtime ratio, per probe"
+    del sink, clocks, sums
+    return {"stream_read": {"GBps": round(read_gbs, 1), "frac_of_peak": round(read_gbs / HBM_PEAK_GBS, 4),
+                            "bytes": nread, "blocks": READ_PROBE_BLOCKS, "loads_in_flight_per_lane": 16},
+            "valu": valu}
 
 
 def copy_calibration(dev):

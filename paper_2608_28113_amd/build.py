@@ -1,4 +1,6 @@
-"""Builds libhscale.so (gfx950) in-tree with hipcc.
+"""Builds libhscale.so (gfx950) in-tree with hipcc, and beside it
+libhscale_probes.so, the benchmark's measurement probes (no part of the
+hscale C ABI).
 
 Flags that fix the arithmetic: -ffp-contract=off (no implicit FMA),
 -fhip-fp32-correctly-rounded-divide-sqrt (IEEE division), and packed-FP32
@@ -17,6 +19,8 @@ CSRC = PKG / "csrc"
 SOURCES = [CSRC / "hdiag.hip", CSRC / "search.hip", CSRC / "diag.hip"]  # share csrc/common.h
 INCLUDE = ROOT / "include"
 LIB = PKG / "libhscale.so"
+PROBE_SOURCES = [CSRC / "probes.hip"]
+PROBE_LIB = PKG / "libhscale_probes.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -27,9 +31,9 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> Path:
-    tmp = LIB.with_suffix(".so.tmp%d" % os.getpid())
-    cmd = [HIPCC, *FLAGS, "-I", str(INCLUDE), "-I", str(CSRC), "-o", str(tmp), *map(str, SOURCES)]
+def _hipcc(sources, out: Path, verbose: bool) -> Path:
+    tmp = out.with_suffix(".so.tmp%d" % os.getpid())
+    cmd = [HIPCC, *FLAGS, "-I", str(INCLUDE), "-I", str(CSRC), "-o", str(tmp), *map(str, sources)]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -39,8 +43,13 @@ def build(verbose: bool = False) -> Path:
         raise RuntimeError("hipcc failed:\n" + err)
     if err and verbose:
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> Path:
+    _hipcc(PROBE_SOURCES, PROBE_LIB, verbose)
+    return _hipcc(SOURCES, LIB, verbose)
 
 
 if __name__ == "__main__":
