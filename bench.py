@@ -305,13 +305,18 @@ def main():
         progress("measured ceilings (streaming read, VALU issue)")
         ceil = ceilings_leg(max(acts.values(), key=lambda X: X.numel()), stream)
         rl_hdiag["frac_of_stream_read"] = round(hd_gbs / ceil["stream_read"]["GBps"], 4)
-        wc = sum(W.numel() * (2 * w + 1 if w is not None else args.down + args.up + 1)
-                 for (_, W, _, _, w) in layers)
-        mix = ceil["valu"]["search_pair_weight_candidates_per_s"]
+        Ks = [2 * w + 1 if w is not None else args.down + args.up + 1 for (_, _, _, _, w) in layers]
+        wc = sum(W.numel() * K for (_, W, _, _, _), K in zip(layers, Ks))
         rl_search["weight_candidates_per_s"] = wc / t_s.mean()
-        rl_search["frac_of_search_mix"] = round(wc / t_s.mean() / mix, 4)
-        if iso is not None:
-            rl_search["frac_of_search_mix_isolated"] = round(wc / iso / mix, 4)
+        walk = ("class" if all(CLASS_WALK_K[0] <= K <= CLASS_WALK_K[1] for K in Ks)
+                else "plain" if all(K < CLASS_WALK_K[0] for K in Ks) else None)
+        if walk is not None:
+            probe = "search_class_pair" if walk == "class" else "search_pair"
+            mix = ceil["valu"][f"{probe}_weight_candidates_per_s"]
+            rl_search["search_mix_probe"] = probe
+            rl_search["frac_of_search_mix"] = round(wc / t_s.mean() / mix, 4)
+            if iso is not None:
+                rl_search["frac_of_search_mix_isolated"] = round(wc / iso / mix, 4)
     default_shape = args.init == "maxabs" and args.down is None and args.window is None
     traffic = measured_traffic(args.workload) if default_shape else None
     if traffic:
@@ -406,7 +411,11 @@ def load_probes():
 
 # hsprobe_valu kinds: (name, loop iterations, VALU instructions per iteration)
 VALU_PROBES = {0: ("fma", 1024, 64), 1: ("pack_cvt", 256, 64), 2: ("unpack_cvt", 512, 64),
-               3: ("search_pair", 512, None)}
+               3: ("search_pair", 512, None), 4: ("search_class_pair", 512, None)}
+# Windows of this many candidates take the search's residue-class walk (when
+# every lane of a wave has only normal, unclipped candidates); fewer take the
+# plain walk.  Each is set against the probe of its own instruction stream.
+CLASS_WALK_K = (16, 24)
 READ_PROBE_BLOCKS = 1792  # as many blocks as the chip keeps resident (256 CUs x 7)
 
 
@@ -421,9 +430,13 @@ def ceilings_leg(X, stream):
                    instruction per SIMD at the clock read from s_memtime /
                    s_memrealtime), and the scale search's per-candidate
                    instruction stream (two candidates of a 16-weight group per
-                   iteration), whose weight-candidates per second the search's
-                   own rate is set against (frac_of_search_mix).  7 waves per
-                   SIMD, the search kernel's occupancy."""
+                   iteration; and the residue-class walk's stream for two
+                   members of one class), whose weight-candidates per second
+                   the search's own rate is set against (frac_of_search_mix,
+                   against the stream of the walk its windows take; max-abs
+                   and 4over6 initial codes alike, so 4over6's extra per-group
+                   work shows as a lower fraction).  7 waves per SIMD, the
+                   search kernel's occupancy."""
     import torch
 
     lib = load_probes()
@@ -469,8 +482,8 @@ def ceilings_leg(X, stream):
             if name == "fma":
                 valu["fma_T_lane_ops_per_s"] = round(blocks * 256 * iters * per_iter / t / 1e12, 2)
         else:
-            valu["search_pair_weight_candidates_per_s"] = blocks * 256 * iters * 2 * 16 / t
-            valu["search_pair_ms"] = round(t * 1e3, 4)
+            valu[f"{name}_weight_candidates_per_s"] = blocks * 256 * iters * 2 * 16 / t
+            valu[f"{name}_ms"] = round(t * 1e3, 4)
     valu["clock_GHz"] = [round(g, 3) for g in ghz]
     valu["clock_source"] = "median over waves of the s_memtime / s_memrealtime ratio, per probe"
     del sink, clocks, sums

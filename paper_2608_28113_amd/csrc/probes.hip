@@ -26,7 +26,11 @@
 //                             16 products w R and 8 pack conversions, 8 unpack
 //                             conversions, 16 residual FMAs, 16 products h r,
 //                             16 accumulating FMAs, 3 adds, then the
-//                             first-minimum update
+//                             first-minimum update (the plain walk)
+//                          4  the same for the two members c and c + 8 of one
+//                             residue class (the residue-class walk): the 16
+//                             products once, converted at scale operands 1
+//                             and 2
 //                        sink[lane] receives a value that depends on the whole
 //                        loop.  Returns 0, or -1 for a bad kind or size.
 //   hsprobe_wall_clock_khz  frequency of s_memrealtime (device 0).
@@ -92,6 +96,27 @@ __device__ __forceinline__ uint2 pack16(const float (&w)[16], float R, uint2 p) 
     return p;
 }
 
+// Two candidates of one residue class (codes c and c + 8, reciprocal scales R
+// and R / 2) from one set of products: the conversion's power-of-two scale
+// operand 2 halves each product before rounding.
+template <int K>
+__device__ __forceinline__ void pack_pair_class(const float (&w)[16], float R, uint32_t &word1, uint32_t &word2) {
+    const float x0 = mul_e64(w[2 * K], R), x1 = mul_e64(w[2 * K + 1], R);
+    word1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word1, x0, x1, 1.0f, K & 3);
+    word2 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word2, x0, x1, 2.0f, K & 3);
+}
+
+__device__ __forceinline__ void pack16_class(const float (&w)[16], float R, uint2 &p, uint2 &q) {
+    pack_pair_class<0>(w, R, p.x, q.x);
+    pack_pair_class<1>(w, R, p.x, q.x);
+    pack_pair_class<2>(w, R, p.x, q.x);
+    pack_pair_class<3>(w, R, p.x, q.x);
+    pack_pair_class<4>(w, R, p.y, q.y);
+    pack_pair_class<5>(w, R, p.y, q.y);
+    pack_pair_class<6>(w, R, p.y, q.y);
+    pack_pair_class<7>(w, R, p.y, q.y);
+}
+
 template <int K>
 __device__ __forceinline__ void error_pair(const float (&w)[16], const float (&h)[16], uint32_t word, float S,
                                            float (&e)[4]) {
@@ -154,11 +179,12 @@ __global__ __launch_bounds__(kThreads) void valu_kernel(int iters, float seed, f
         h[j] = 1.0f + (float)((lane * 3 + j) % 7);
     }
     float Ra = 0.9f, Rb = 1.1f, Sa = 1.0f / 0.9f, Sb = 1.0f / 1.1f;
+    if constexpr (kKind == 4) Sb = 2.0f * Sa;  // the class member c + 8
     float best = INFINITY;
     int best_d = 0;
     uint2 pa = make_uint2(0u, 0u), pb = pa, bp = pa;
     // Materialise the set-up before the first clock read.
-    if constexpr (kKind == 3) {
+    if constexpr (kKind >= 3) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) asm volatile("" : "+v"(w[j]), "+v"(h[j]));
     }
@@ -191,8 +217,12 @@ __global__ __launch_bounds__(kThreads) void valu_kernel(int iters, float seed, f
             // The scales pass through an empty asm statement each iteration,
             // so no candidate's work can be hoisted out of the loop.
             asm volatile("" : "+v"(Ra), "+v"(Rb), "+v"(Sa), "+v"(Sb));
-            pa = pack16(w, Ra, pa);
-            pb = pack16(w, Rb, pb);
+            if constexpr (kKind == 3) {
+                pa = pack16(w, Ra, pa);
+                pb = pack16(w, Rb, pb);
+            } else {
+                pack16_class(w, Ra, pa, pb);
+            }
             const float ea = error16(w, h, pa, Sa);
             const float eb = error16(w, h, pb, Sb);
             if (ea < best) {
@@ -246,6 +276,7 @@ extern "C" int hsprobe_valu(int32_t kind, int32_t blocks, int32_t iters, float *
         case 1: k = valu_kernel<1>; break;
         case 2: k = valu_kernel<2>; break;
         case 3: k = valu_kernel<3>; break;
+        case 4: k = valu_kernel<4>; break;
         default: return -1;
     }
     hipLaunchKernelGGL(k, dim3(blocks), dim3(kThreads), 0, stream, iters, 1.0f, sink, clocks);

@@ -37,7 +37,7 @@ def test_probe_arguments_are_checked_on_the_host(P):
     assert P.hsprobe_stream_read(fake, 0, 4, fake, None) == -1
     assert P.hsprobe_stream_read(fake, 1 << 20, 0, fake, None) == -1
     assert P.hsprobe_stream_read(fake, 65535 * 4, 4, fake, None) == -1  # under one 64 KiB round per block
-    for kind in (-1, 4):
+    for kind in (-1, 5):
         assert P.hsprobe_valu(kind, 8, 16, fake, fake, None) == -1
     assert P.hsprobe_valu(0, 0, 16, fake, fake, None) == -1
     assert P.hsprobe_valu(0, 8, 0, fake, fake, None) == -1
@@ -65,7 +65,7 @@ def test_stream_read_reads_every_byte(P):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("kind", [0, 1, 2, 3])
+@pytest.mark.parametrize("kind", [0, 1, 2, 3, 4])
 def test_valu_probe_runs_and_records_clocks(P, kind):
     import torch
     blocks = 16
