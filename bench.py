@@ -444,16 +444,19 @@ def ceilings_leg(X, stream):
     simds = 4 * cus
 
     def timed(fn, runs):
-        ts, r = [], None
-        for i in range(runs + 1):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            r = fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            if i:  # the first run is a warm-up
-                ts.append(e0.elapsed_time(e1) * 1e-3)
-        return float(np.median(ts)), r
+        # A warm-up run, then `runs` runs queued back to back with an event
+        # between each two: the GPU is busy when each event is reached, so an
+        # interval holds one kernel and none of the host's launch latency.
+        statuses = [fn()]
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(runs + 1)]
+        evs[0].record(stream)
+        for i in range(runs):
+            statuses.append(fn())
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ts = [evs[i].elapsed_time(evs[i + 1]) * 1e-3 for i in range(runs)]
+        bad = [s for s in statuses if s < 0]
+        return float(np.median(ts)), (bad[0] if bad else statuses[-1])
 
     sums = torch.empty(READ_PROBE_BLOCKS * 256, dtype=torch.int32, device=X.device)
     t_read, nread = timed(lambda: lib.hsprobe_stream_read(X.data_ptr(), X.numel() * X.element_size(),
@@ -476,6 +479,7 @@ def ceilings_leg(X, stream):
         c = clocks.view(-1, 4).cpu().numpy().astype(np.float64)
         clock = float(np.median((c[:, 1] - c[:, 0]) / (c[:, 3] - c[:, 2]))) * wall_hz
         ghz.append(clock / 1e9)
+        valu[f"{name}_ms"] = round(t * 1e3, 4)
         if per_iter is not None:
             instr_per_simd = blocks * 4 * iters * per_iter / simds
             valu[f"{name}_cycles_per_instr_per_simd"] = round(t * clock / instr_per_simd, 3)
@@ -483,12 +487,11 @@ def ceilings_leg(X, stream):
                 valu["fma_T_lane_ops_per_s"] = round(blocks * 256 * iters * per_iter / t / 1e12, 2)
         else:
             valu[f"{name}_weight_candidates_per_s"] = blocks * 256 * iters * 2 * 16 / t
-            valu[f"{name}_ms"] = round(t * 1e3, 4)
     valu["clock_GHz"] = [round(g, 3) for g in ghz]
     valu["clock_source"] = "median over waves of the s_memtime / s_memrealtime ratio, per probe"
     del sink, clocks, sums
     return {"stream_read": {"GBps": round(read_gbs, 1), "frac_of_peak": round(read_gbs / HBM_PEAK_GBS, 4),
-                            "bytes": nread, "blocks": READ_PROBE_BLOCKS, "loads_in_flight_per_lane": 16},
+                            "ms": round(t_read * 1e3, 4), "bytes": nread, "blocks": READ_PROBE_BLOCKS, "loads_in_flight_per_lane": 16},
             "valu": valu}
 
 
