@@ -52,3 +52,24 @@ def test_committed_profile_traffic_matches_the_algorithmic_bytes(workload):
         weights = wl.out * wl.inp
     assert abs(t["hdiag"] / hd - 1) < 0.01, (t["hdiag"], hd)
     assert abs(t["search"] / (bench.SEARCH_BYTES_PER_WEIGHT * weights) - 1) < 0.01
+
+
+def test_committed_diagnostics_profile_is_current():
+    """The output-error summary the diagnostics leg quotes as `traffic` was
+    collected on the current output-error kernel sources."""
+    import bench
+    t = bench.diag_traffic("down_proj")
+    assert t is not None, "profiles/output_error_down_proj.json is absent or older than the kernel sources"
+
+
+def test_committed_ceilings_profile_is_current():
+    """profiles/ceilings_down_proj.md (the probe kernels' trace beside the
+    bench's timings) names the source hash of csrc/probes.hip it was taken
+    on; it must be the current one."""
+    import hashlib
+    import re
+    text = (ROOT / "profiles" / "ceilings_down_proj.md").read_text()
+    m = re.search(r"csrc/probes\.hip at collection: `([0-9a-f]{16})`", text)
+    assert m, "the summary names no source hash"
+    src = (ROOT / "paper_2608_28113_amd" / "csrc" / "probes.hip").read_bytes()
+    assert m.group(1) == hashlib.sha256(src).hexdigest()[:16], "re-collect the ceilings profile"
