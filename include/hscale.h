@@ -148,7 +148,9 @@ int hscale_hdiag(const void *X, int64_t tokens, int64_t in, float *h,
  * All calls on one GPU share that GPU's array: calls that may run at the
  * same time on one GPU (different streams, or host threads that do not
  * order their streams) race on it and give undefined h.  Calls ordered on
- * one stream are safe; nothing is carried from one call to the next.
+ * one stream are safe: every partial a call reads is written earlier in the
+ * same call, so the array needs no clearing and nothing is carried from one
+ * call to the next.
  */
 int hscale_hdiag_noalloc(const void *X, int64_t tokens, int64_t in, float *h,
                          hipStream_t stream);
