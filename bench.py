@@ -293,13 +293,21 @@ def main():
                 "kernel": "hscale_hdiag (hdiag_partial + hdiag_tree)",
                 "algorithmic_bytes_per_step": hd_bytes, "avg_ms_per_step": round(t_h.mean() * 1e3, 4),
                 "launches_per_step": nh}
+    # The model's bound: VALU for windows of a few candidates and up, HBM for
+    # the smallest (window 0, the RTN baseline, moves 2.56 bytes but issues
+    # only 8 ops per weight).
+    valu_bound = ops / (VALU_PEAK_TOPS * 1e12) >= SEARCH_BYTES_PER_WEIGHT * weights / (HBM_PEAK_GBS * 1e9)
     rl_search = {"bound": "alu", "achieved": round(search_tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
                  "unit": "T lane-ops/s", "frac": round(search_tops / VALU_PEAK_TOPS, 4), "traffic": None,
                  "kernel": "hscale_search (search_kernel)",
                  "algorithmic_ops_per_step": ops, "hbm_GBps": round(search_gbs, 1),
-                 "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
+                 "hbm_frac": round(search_gbs / HBM_PEAK_GBS, 4), "valu_frac": round(search_tops / VALU_PEAK_TOPS, 4),
+                 "avg_ms_per_step": round(t_s.mean() * 1e3, 4),
                  "launches_per_step": 1 if len(layers) <= 32 else (len(layers) + 31) // 32,
                  "layers": len(layers)}
+    if not valu_bound:
+        rl_search.update({"bound": "hbm", "achieved": round(search_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(search_gbs / HBM_PEAK_GBS, 4)})
     ceil = None
     if not args.no_ceilings:
         progress("measured ceilings (streaming read, VALU issue)")
@@ -310,7 +318,7 @@ def main():
         rl_search["weight_candidates_per_s"] = wc / t_s.mean()
         walk = ("class" if all(CLASS_WALK_K[0] <= K <= CLASS_WALK_K[1] for K in Ks)
                 else "plain" if all(K < CLASS_WALK_K[0] for K in Ks) else None)
-        if walk is not None:
+        if walk is not None and valu_bound:
             probe = "search_class_pair" if walk == "class" else "search_pair"
             mix = ceil["valu"][f"{probe}_weight_candidates_per_s"]
             rl_search["search_mix_probe"] = probe

@@ -175,7 +175,8 @@ int hscale_hdiag_finalize(const double *h64, int64_t in, float *h,
 /*
  * The per-group NVFP4 scale search of Sec. 3.3 (Eq. 7, 9-13) with the
  * symmetric shift set d = -window .. +window (K = 2 window + 1 candidates).
- * window == 0 is the plain max-abs (RTN) scale of Eq. 7.
+ * window == 0 is the plain max-abs (RTN) scale of Eq. 7; a single candidate
+ * needs no score, so h is then not read (it must still be a valid pointer).
  *
  * W             bf16 [out, in], row-major, 16-byte aligned.  Group (r, i)
  *               is W[r, 16 i .. 16 i + 15].

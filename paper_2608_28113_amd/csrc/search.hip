@@ -164,34 +164,37 @@ __device__ __forceinline__ void quantize_group_multi(const float (&w)[kGroup], f
 // the 9-candidate one loses 4%).
 constexpr int kClassMinCandidates = 16;
 
-// Eq. 7 and 9-13 for one group held in registers: the initial code (by the
-// rule kInit; `given` is the caller's code for kInitGiven), then the walk
-// d = -down..up, keeping the first minimum.  With kStats it also reports the
-// chosen shift, its error and the error at d = 0.
+// The initial code of Eq. 7 by the rule kInit (`given` is the caller's code
+// for kInitGiven), in 1..126.
+template <int kInit>
+__device__ __forceinline__ int initial_code(const float (&w)[kGroup], const ScaleEntry *tab, float s_g, int given) {
+    if (kInit == kInitGiven) return min(max(given, 1), kMaxCode);
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
+    int c0 = anchor_code(amax, 6.0f, s_g);
+    if (kInit == kInitFourOverSix) {
+        // Anchor 4 (amax / 4 is exact) against anchor 6 by plain squared
+        // error; anchor 4 on a tie.
+        const int c4 = anchor_code(amax, 4.0f, s_g);
+        const ScaleEntry e4 = tab[c4 + kTabPad];
+        const ScaleEntry e6 = tab[c0 + kTabPad];
+        const float l4 = group_plain_error(w, quantize_group(w, e4.R, make_uint2(0u, 0u)), e4.S);
+        const float l6 = group_plain_error(w, quantize_group(w, e6.R, make_uint2(0u, 0u)), e6.S);
+        if (l4 <= l6) c0 = c4;
+    }
+    return c0;
+}
+
+// Eq. 7 and 9-13 for one group held in registers: the initial code, then the
+// walk d = -down..up, keeping the first minimum.  With kStats it also
+// reports the chosen shift, its error and the error at d = 0.
 template <int kInit, bool kStats>
 __device__ __forceinline__ void search_group(const float (&w)[kGroup], const float (&hh)[kGroup],
                                              const ScaleEntry *tab, int down, int up, float s_g, int given,
                                              int &code, uint2 &best_p, int &shift, float &err_best,
                                              float &err_init) {
-    int c0;
-    if (kInit == kInitGiven) {
-        c0 = min(max(given, 1), kMaxCode);
-    } else {
-        float amax = 0.0f;
-#pragma unroll
-        for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(w[j]));
-        c0 = anchor_code(amax, 6.0f, s_g);
-        if (kInit == kInitFourOverSix) {
-            // Anchor 4 (amax / 4 is exact) against anchor 6 by plain squared
-            // error; anchor 4 on a tie.
-            const int c4 = anchor_code(amax, 4.0f, s_g);
-            const ScaleEntry e4 = tab[c4 + kTabPad];
-            const ScaleEntry e6 = tab[c0 + kTabPad];
-            const float l4 = group_plain_error(w, quantize_group(w, e4.R, make_uint2(0u, 0u)), e4.S);
-            const float l6 = group_plain_error(w, quantize_group(w, e6.R, make_uint2(0u, 0u)), e6.S);
-            if (l4 <= l6) c0 = c4;
-        }
-    }
+    const int c0 = initial_code<kInit>(w, tab, s_g, given);
     const ScaleEntry *col = tab + (c0 + kTabPad);  // col[d] is candidate c0 + d, clipped
     const int K = down + up + 1;
     if (K >= kClassMinCandidates && K <= 24 && __all(c0 - down >= 8 && c0 + up <= kMaxCode)) {
@@ -343,6 +346,7 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
         ++r;
     }
     const uint32_t step_r = stride / a.Gc, step_i = stride % a.Gc;
+    const bool single = a.down == 0 && a.up == 0;  // wave-uniform
 
     for (;;) {
         float w[kGroup];
@@ -352,22 +356,30 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
         } else {
             load_group(a.W + (uint64_t)r * a.ldw_vec + 2 * (uint64_t)i, 0, w);
         }
-        float hh[kGroup];
-        const float4 *hsrc = kFlat ? at_byte(a.h, i << 6) : a.h + 4 * (uint64_t)i;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float4 v = hsrc[q];
-            hh[4 * q] = v.x;
-            hh[4 * q + 1] = v.y;
-            hh[4 * q + 2] = v.z;
-            hh[4 * q + 3] = v.w;
-        }
         int given = 0;
         if (kInit == kInitGiven) given = kFlat ? (int)*at_byte(a.init, g) : (int)a.init[(uint64_t)r * a.ldi + i];
-        int code, shift;
+        int code, shift = 0;
         uint2 best_p;
-        float e_best, e_init;
-        search_group<kInit, kStats>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p, shift, e_best, e_init);
+        float e_best = 0.0f, e_init = 0.0f;
+        if (!kStats && single) {
+            // One candidate is its own first minimum: it needs no score, so
+            // h is not read (the RTN code of Eq. 7 and its quantization).
+            code = initial_code<kInit>(w, tab, a.s_g, given);
+            best_p = quantize_group(w, tab[code + kTabPad].R, make_uint2(0u, 0u));
+        } else {
+            float hh[kGroup];
+            const float4 *hsrc = kFlat ? at_byte(a.h, i << 6) : a.h + 4 * (uint64_t)i;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 v = hsrc[q];
+                hh[4 * q] = v.x;
+                hh[4 * q + 1] = v.y;
+                hh[4 * q + 2] = v.z;
+                hh[4 * q + 3] = v.w;
+            }
+            search_group<kInit, kStats>(w, hh, tab, a.down, a.up, a.s_g, given, code, best_p, shift, e_best,
+                                        e_init);
+        }
         if (kFlat) {
             *at_byte(a.codes, g) = (uint8_t)code;
             *at_byte(a.packed, g << 3) = best_p;
@@ -443,22 +455,28 @@ __global__ __launch_bounds__(kSearchThreads) void search_layers_kernel(const Bat
     } else {
         load_group(ly.W, g, w);
     }
-    float hh[kGroup];
-    const float4 *hsrc = kFlat ? at_byte(ly.h, i << 6) : ly.h + 4 * (uint64_t)i;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const float4 v = hsrc[q];
-        hh[4 * q] = v.x;
-        hh[4 * q + 1] = v.y;
-        hh[4 * q + 2] = v.z;
-        hh[4 * q + 3] = v.w;
-    }
     int given = 0;
     if (kInit == kInitGiven) given = kFlat ? (int)*at_byte(ly.init, g) : (int)ly.init[g];
-    int code, shift;
+    int code;
     uint2 best_p;
-    float e_best, e_init;
-    search_group<kInit, false>(w, hh, tab, a.down, a.up, ly.s_g, given, code, best_p, shift, e_best, e_init);
+    if (a.down == 0 && a.up == 0) {  // one candidate: no score, h not read
+        code = initial_code<kInit>(w, tab, ly.s_g, given);
+        best_p = quantize_group(w, tab[code + kTabPad].R, make_uint2(0u, 0u));
+    } else {
+        float hh[kGroup];
+        const float4 *hsrc = kFlat ? at_byte(ly.h, i << 6) : ly.h + 4 * (uint64_t)i;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = hsrc[q];
+            hh[4 * q] = v.x;
+            hh[4 * q + 1] = v.y;
+            hh[4 * q + 2] = v.z;
+            hh[4 * q + 3] = v.w;
+        }
+        int shift;
+        float e_best, e_init;
+        search_group<kInit, false>(w, hh, tab, a.down, a.up, ly.s_g, given, code, best_p, shift, e_best, e_init);
+    }
     if (kFlat) {
         *at_byte(ly.codes, g) = (uint8_t)code;
         *at_byte(ly.packed, g << 3) = best_p;
