@@ -297,8 +297,11 @@ def group_search(w, h, s_g: float, down: int, up: int):
 
 def near_tie_mask(e_best: np.ndarray, e_second: np.ndarray, rel: float = NEAR_TIE_REL):
     """Groups whose best and second-best distinct-code errors are within
-    ``rel`` (relative to the second); two zero errors count as a tie."""
-    return (e_second - e_best) <= rel * e_second
+    ``rel`` (relative to the second); two zero errors count as a tie.  A
+    window with a single distinct code (window 0, or every candidate clipped
+    to one end of the ladder) has no second-best (+inf) and no tie."""
+    e_second = np.asarray(e_second, np.float64)
+    return np.isfinite(e_second) & ((e_second - e_best) <= rel * e_second)
 
 
 def pack_nibbles(nib: np.ndarray) -> np.ndarray:

@@ -330,3 +330,18 @@ def test_zero_group_and_saturation():
     w = np.full(16, 2.0 ** -20, np.float32)
     r = oracle.search(_bits(w).reshape(1, 16), h, 1.0, window=0)
     assert r["codes"][0, 0] == 1
+
+
+def test_single_distinct_code_is_no_tie():
+    # With one distinct candidate code there is no second-best error: window
+    # 0, and a saturated group whose upward shifts all clip to code 126.
+    rng = np.random.default_rng(3)
+    u32 = (rng.standard_normal((4, 64)) * 0.02).astype(np.float32).view(np.uint32)
+    w = ((u32 + 0x7FFF + ((u32 >> 16) & 1)) & 0xFFFF0000).astype(np.uint32).view(np.float32)  # to bf16
+    h = np.ones(64, np.float32)
+    r = oracle.search(_bits(w), h, float(np.float32(np.abs(w).max() / 2688)), window=0)
+    assert np.all(np.isinf(r["e_second"])) and not oracle.near_tie_mask(r["e_best"], r["e_second"]).any()
+    w = np.full(16, 1.0, np.float32)
+    r = oracle.search(_bits(w).reshape(1, 16), np.ones(16, np.float32), 1e-6, down=0, up=3)
+    assert r["codes"][0, 0] == 126 and np.isinf(r["e_second"][0, 0])
+    assert not oracle.near_tie_mask(r["e_best"], r["e_second"])[0, 0]
