@@ -331,7 +331,13 @@ template <int kInit, bool kStats, bool kFlat>
 __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs a) {
     __shared__ ScaleEntry tab[kTabSize];
     __shared__ ScaleEntry uniq[kMaxCode + 1];
-    build_scale_table(tab, uniq, a.s_g);
+    const bool single = a.down == 0 && a.up == 0;  // wave-uniform
+    // A single candidate under the max-abs or given rule needs one scale per
+    // lane, computed directly (the same fp32 product and correctly rounded
+    // reciprocal as the table's entry); every other search reads the block's
+    // table.
+    const bool direct = !kStats && single && kInit != kInitFourOverSix;
+    if (!direct) build_scale_table(tab, uniq, a.s_g);
 
     const uint32_t stride = gridDim.x * kSearchThreads;
     const uint32_t first = blockIdx.x * kSearchThreads;  // wave-uniform
@@ -346,7 +352,6 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
         ++r;
     }
     const uint32_t step_r = stride / a.Gc, step_i = stride % a.Gc;
-    const bool single = a.down == 0 && a.up == 0;  // wave-uniform
 
     for (;;) {
         float w[kGroup];
@@ -365,7 +370,8 @@ __global__ __launch_bounds__(kSearchThreads) void search_kernel(const SearchArgs
             // One candidate is its own first minimum: it needs no score, so
             // h is not read (the RTN code of Eq. 7 and its quantization).
             code = initial_code<kInit>(w, tab, a.s_g, given);
-            best_p = quantize_group(w, tab[code + kTabPad].R, make_uint2(0u, 0u));
+            const float R = direct ? 1.0f / (a.s_g * e4m3fn_value(code)) : tab[code + kTabPad].R;
+            best_p = quantize_group(w, R, make_uint2(0u, 0u));
         } else {
             float hh[kGroup];
             const float4 *hsrc = kFlat ? at_byte(a.h, i << 6) : a.h + 4 * (uint64_t)i;
@@ -440,7 +446,9 @@ __global__ __launch_bounds__(kSearchThreads) void search_layers_kernel(const Bat
     const BatchLayer ly = a.layer[L];
     __shared__ ScaleEntry tab[kTabSize];
     __shared__ ScaleEntry uniq[kMaxCode + 1];
-    build_scale_table(tab, uniq, ly.s_g);
+    const bool single = a.down == 0 && a.up == 0;
+    const bool direct = single && kInit != kInitFourOverSix;  // as in search_kernel
+    if (!direct) build_scale_table(tab, uniq, ly.s_g);
 
     const uint32_t first = (blockIdx.x - ly.block0) * kSearchThreads;  // wave-uniform
     const uint32_t g = first + threadIdx.x;
@@ -459,9 +467,10 @@ __global__ __launch_bounds__(kSearchThreads) void search_layers_kernel(const Bat
     if (kInit == kInitGiven) given = kFlat ? (int)*at_byte(ly.init, g) : (int)ly.init[g];
     int code;
     uint2 best_p;
-    if (a.down == 0 && a.up == 0) {  // one candidate: no score, h not read
+    if (single) {  // one candidate: no score, h not read
         code = initial_code<kInit>(w, tab, ly.s_g, given);
-        best_p = quantize_group(w, tab[code + kTabPad].R, make_uint2(0u, 0u));
+        const float R = direct ? 1.0f / (ly.s_g * e4m3fn_value(code)) : tab[code + kTabPad].R;
+        best_p = quantize_group(w, R, make_uint2(0u, 0u));
     } else {
         float hh[kGroup];
         const float4 *hsrc = kFlat ? at_byte(ly.h, i << 6) : ly.h + 4 * (uint64_t)i;
